@@ -1,0 +1,254 @@
+"""Benchmark: batched paged GQA decode attention on one MI355X.
+
+One step = one call of the whole path (plan, decode, combine kernels) over one
+batch: every request of the batch decodes one token through one attention
+layer. The default workload is the Llama-3-8B layer shape (32 q heads, 8 kv
+heads, head_dim 128, block 16), batch 64, lengths uniform in [512, 2048],
+shuffled physical blocks, bf16 q/K/V ~ N(0,1) (synthetic, seeded).
+
+Inputs are resident in HBM before timing. The KV cache is replicated enough
+times that consecutive steps never find their data in the 256 MB Infinity
+Cache (each replica holds identical values). Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--config N] [--variant auto|valu|mfma]
+    python bench.py --copy-calibration     # plain copy of known size, for rocprofv3 --pmc
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
+MALL_BYTES = 256 * 2 ** 20     # Infinity Cache
+METRIC = "decode-attention achieved HBM GB/s (% of peak) + tokens/sec per layer, 1 GPU"
+KERNEL_SOURCES = ("decode_mfma.hip", "decode_valu.hip", "decode_common.h", "neo_internal.h")
+SEQ_DESC = {1: "U[64,512]", 2: "U[512,2048]", 3: "lognormal(median 1500, sigma 0.6) clip [128,8192]",
+            4: "U[256,4096]", 5: "8 x 32768 + 1016 x U[16,256]"}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha(variant: str) -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        if name.startswith("decode_") and variant not in name and name != "decode_common.h":
+            continue
+        with open(os.path.join(ROOT, "paper_2411_01142_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload_key: str, variant: str, launches_per_step: int = 1):
+    """HBM bytes per decode launch from committed rocprofv3 --pmc summaries, or None
+    when they are missing or were taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"counters_{workload_key}_{variant}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"TRAFFIC_JSON:\s*(\{.*\})", open(path).read())
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("kernel_sha") != kernel_source_sha(variant):
+        return None
+    return float(rec["traffic_bytes_per_launch"])
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch loaded (same soname)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so.7")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        rc = self.lib.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed: {rc}")
+        return ev
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        rc = self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return float(ms.value)
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
+
+
+def cpu_baseline(case, min_seconds: float = 10.0):
+    """The fp64 oracle on the host cores over the whole batch, repeated until
+    ``min_seconds`` have passed; same units as the GPU figure."""
+    import oracle
+    threads = oracle.max_threads()
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        oracle.decode_attention(case, threads=0)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    gbs = case.algorithmic_bytes() * passes / el / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"full batch ({case.batch} requests x {case.num_q_heads} heads), "
+                      f"{passes} pass(es) in {el:.1f} s, fp64 naive softmax, OpenMP",
+            "tokens_per_s_per_layer": round(case.batch * passes / el, 2)}
+
+
+def copy_calibration(nbytes: int = 2 ** 30, reps: int = 5):
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--variant", default="auto", choices=["auto", "valu", "mfma"])
+    ap.add_argument("--max-slices", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the decode-attention path needs no "
+              "collective and this build runs on a single MI355X (--gpus 1).", file=sys.stderr)
+        return 2
+
+    import torch
+    if args.copy_calibration:
+        copy_calibration()
+        return 0
+
+    import paper_2411_01142_amd as neo
+    from paper_2411_01142_amd import workloads as W
+
+    seed = args.config if args.seed is None else args.seed
+    log(f"[bench] generating config {args.config} seed {seed}")
+    case = W.make_config(args.config, seed, poison=False)
+    workload_key = f"cfg{args.config}"
+    q, k, v, bt, sl = case.to_torch("cuda")
+    kv_bytes = k.numel() * 2 + v.numel() * 2
+    nrep = max(1, math.ceil(4 * MALL_BYTES / kv_bytes))
+    reps = [(k, v)] + [(k.clone(), v.clone()) for _ in range(nrep - 1)]
+    out = torch.empty((case.batch, case.num_q_heads, case.head_dim), dtype=torch.float32,
+                      device="cuda")
+    ws = torch.empty(neo.workspace_bytes(case.batch, case.num_q_heads, case.num_kv_heads),
+                     dtype=torch.uint8, device="cuda")
+    lib = neo.load_library()
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    variant_id = neo.VARIANTS[args.variant]
+    resolved = "mfma" if args.variant == "auto" else args.variant
+    hip = HipEvents()
+    ev = [(hip.create(), hip.create()) for _ in range(args.steps)]
+
+    def step(i, evs=(None, None)):
+        kk, vv = reps[i % nrep]
+        rc = lib.neo_decode_attention_events(
+            q.data_ptr(), kk.data_ptr(), vv.data_ptr(), bt.data_ptr(), sl.data_ptr(),
+            case.num_q_heads, case.num_kv_heads, case.head_dim, case.block_size,
+            float(case.scale), out.data_ptr(), case.batch, case.max_blocks_per_seq,
+            case.num_blocks, ws.data_ptr(), ws.numel(), variant_id, args.max_slices,
+            evs[0], evs[1], sh)
+        if rc != 0:
+            raise neo.NeoError(rc, lib.neo_last_error().decode())
+
+    log(f"[bench] {case.name}: B={case.batch} sumL={case.total_tokens()} "
+        f"KV={kv_bytes / 1e6:.1f} MB x{nrep} replicas; warmup {args.warmup}")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, ev[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    decode_ms = [hip.elapsed_ms(a, b) for a, b in ev]
+    for a, b in ev:
+        hip.destroy(a)
+        hip.destroy(b)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    alg_bytes = case.algorithmic_bytes()
+    value = alg_bytes / (ms_per_step * 1e-3) / 1e9
+    dec_ms = sum(decode_ms) / len(decode_ms)
+    achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
+    traffic = load_traffic(workload_key, resolved)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "accumulate": "fp32",
+        "data": "synthetic",
+        "pct_of_peak": round(100.0 * value / PEAK_HBM_GBS, 2),
+        "tokens_per_s_per_layer": round(case.batch / (ms_per_step * 1e-3), 1),
+        "config": {
+            "workload": f"{case.name}: decode attention, {case.num_q_heads} q heads / "
+                        f"{case.num_kv_heads} kv heads, head_dim {case.head_dim}, block "
+                        f"{case.block_size}, batch {case.batch}, seq_lens {SEQ_DESC[args.config]}",
+            "batch": case.batch, "num_q_heads": case.num_q_heads,
+            "num_kv_heads": case.num_kv_heads, "head_dim": case.head_dim,
+            "block_size": case.block_size, "sum_seq_len": case.total_tokens(),
+            "algorithmic_bytes_per_step": alg_bytes, "kv_replicas": nrep,
+            "variant": resolved, "max_slices": args.max_slices,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": f"decode_{resolved}_kernel<{case.group}>",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "kernel_ms": round(dec_ms, 5),
+            "algorithmic_bytes_per_launch": alg_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] CPU baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

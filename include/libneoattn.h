@@ -1,0 +1,172 @@
+/*
+ * libneoattn -- batched paged GQA decode attention on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Neo, arXiv 2411.01142, Sec. 2.1-2.2): in the decoding phase each
+ * request contributes one new query token per query head, and that token attends
+ * over every token in the request's KV cache. It is the only step that touches the
+ * KV cache, needs no weights and is bound by memory bandwidth (Sec. 2.2, Sec. 4).
+ * The cache is paged (fixed-size blocks reached through a per-request block table,
+ * Sec. 2.1 and Sec. 4); query heads share KV heads in groups (GQA, Sec. 4). Work is
+ * partitioned along each request's sequence at block granularity and the partial
+ * outputs of a request are aggregated (Sec. 4, after Flash-Decoding); the GPU
+ * attention runs once per iteration over the whole GPU batch (Sec. 3.1), so the
+ * library takes the whole ragged batch in one call.
+ *
+ * For request b with L = seq_lens[b] cached tokens (the token being decoded
+ * included), query head h and kv head g = h / (num_q_heads / num_kv_heads):
+ *
+ *   s_t          = scale * sum_d q[b][h][d] * K[b][g][t][d],        t in [0, L)
+ *   out[b][h][d] = sum_t exp(s_t - max s) * V[b][g][t][d] / sum_t exp(s_t - max s)
+ *
+ * A request with L = 0 gets a zero row. The exp is natural (the kernels use exp2
+ * with log2(e) folded into the scale).
+ *
+ * Storage contract (all device buffers, row-major, no padding):
+ *   q           bf16  [batch][num_q_heads][head_dim]
+ *   k_cache     bf16  [num_blocks][num_kv_heads][head_dim/8][block_size][8]
+ *                     (key of token t, dims 8c..8c+7, at [blk][g][c][t % block_size][:])
+ *   v_cache     bf16  [num_blocks][num_kv_heads][head_dim][block_size]
+ *                     (value of token t, dim d, at [blk][g][d][t % block_size])
+ *   block_table int32 [batch][max_blocks_per_seq]; token t of request b lives in
+ *                     block block_table[b][t / block_size], slot t % block_size.
+ *                     Entries at and past ceil(L/block_size) are never read.
+ *   seq_lens    int32 [batch]
+ *   out         fp32  [batch][num_q_heads][head_dim]; every element is written.
+ * One (block, kv head) tile of K or of V is one contiguous 4 KiB run.
+ *
+ * Supported: head_dim 128, block_size 16, num_q_heads / num_kv_heads in {1,2,4,8,16}.
+ * q, k_cache, v_cache and out must be 16-byte aligned; the workspace 256-byte aligned.
+ *
+ * Ownership: the caller owns every buffer. The library keeps no pointer after a
+ * call returns and allocates nothing on any path.
+ * Asynchrony: calls enqueue kernels on `stream` (a hipStream_t; NULL = the null
+ * stream) and return without synchronising. Device faults surface at the caller's
+ * next synchronisation.
+ * Errors: arguments are checked on the host before any HIP call; a non-OK status
+ * sets a message readable with neo_last_error(). Launch failures return NEO_ERR_HIP.
+ * Block ids outside [0, num_blocks) are clamped to a valid block (no fault, wrong
+ * result); seq_lens above max_blocks_per_seq * block_size are clamped to it and
+ * negative ones read as 0. neo_debug_validate() reports both.
+ * Concurrency: stateless apart from the thread-local error text. Calls that may
+ * overlap on the device need distinct workspaces.
+ */
+#ifndef LIBNEOATTN_H
+#define LIBNEOATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NEO_OK = 0,
+  NEO_ERR_INVALID_ARG = 1, /* null pointer, negative size, num_q_heads % num_kv_heads != 0,
+                              non-finite scale, misaligned buffer, size overflow */
+  NEO_ERR_UNSUPPORTED = 2, /* head_dim != 128, block_size != 16, group not in {1,2,4,8,16},
+                              unknown variant */
+  NEO_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than neo_decode_workspace_bytes() */
+  NEO_ERR_HIP = 4          /* a HIP call or kernel launch failed; detail in neo_last_error() */
+} neo_status;
+
+/* Kernel family for the decode step (neo_decode_attention_ex). */
+typedef enum {
+  NEO_VARIANT_AUTO = 0, /* the fastest measured on MI355X for the group size */
+  NEO_VARIANT_VALU = 1, /* vector-ALU dot products with DPP row reductions */
+  NEO_VARIANT_MFMA = 2  /* q.K and p.V on bf16 matrix cores, query group padded to 16 */
+} neo_variant;
+
+/* Largest number of sequence slices (one wavefront each) a call may use. */
+#define NEO_MAX_SLICES 4096
+
+/*
+ * Bytes of device workspace neo_decode_attention needs: the work plan (slice
+ * starts, per-request tile offsets) and room for two partial outputs per slice
+ * (group * head_dim fp32 values plus group log-sum-exps each). Depends only on
+ * host scalars, so it can be allocated ahead of time. Sized for NEO_MAX_SLICES.
+ */
+neo_status neo_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                      int32_t head_dim, size_t* bytes_out);
+
+/*
+ * Decode attention of the whole ragged batch (the operation and layouts above).
+ * The first eleven arguments follow the problem statement in that order; the rest
+ * are what a device pointer cannot carry: batch size, block-table row stride
+ * (max_blocks_per_seq), pool size (num_blocks), the workspace and the stream.
+ * Enqueues three kernels (plan, decode, combine). Reads q, k_cache, v_cache,
+ * block_table and seq_lens; writes out and the workspace.
+ * batch == 0 is a no-op (pointers may then be NULL).
+ */
+neo_status neo_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const int32_t* seq_lens,
+                                int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                int32_t block_size, float scale, float* out, int32_t batch,
+                                int32_t max_blocks_per_seq, int32_t num_blocks, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/*
+ * As neo_decode_attention, with the kernel family and the number of sequence
+ * slices chosen by the caller. max_slices = 0 picks the library default; any
+ * value in [1, NEO_MAX_SLICES] caps the number of slices the plan may cut
+ * (1 = no request is ever split). The result is the same operation for every
+ * choice, up to fp32 summation order.
+ */
+neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t block_size, float scale, float* out, int32_t batch,
+                                   int32_t max_blocks_per_seq, int32_t num_blocks,
+                                   void* workspace, size_t workspace_bytes, int32_t variant,
+                                   int32_t max_slices, void* stream);
+
+/*
+ * As neo_decode_attention_ex, also recording two caller-created HIP events
+ * (hipEvent_t, may be NULL) on `stream` immediately before and after the decode
+ * kernel, so the main kernel can be timed apart from the plan and combine
+ * launches. Meant for measurement.
+ */
+neo_status neo_decode_attention_events(const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* block_table, const int32_t* seq_lens,
+                                       int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t head_dim, int32_t block_size, float scale,
+                                       float* out, int32_t batch, int32_t max_blocks_per_seq,
+                                       int32_t num_blocks, void* workspace,
+                                       size_t workspace_bytes, int32_t variant,
+                                       int32_t max_slices, void* decode_start_event,
+                                       void* decode_end_event, void* stream);
+
+/*
+ * Bit-exact dense copy of one paged cache through the block table (the paged
+ * layout of Sec. 2.1 / Sec. 4). is_v = 0 reads the K layout, 1 the V layout.
+ * token_offsets: device int32 [batch+1], exclusive prefix sum of seq_lens
+ * (token_offsets[batch] = total). dst: device bf16 [total][num_kv_heads][head_dim],
+ * row token_offsets[b] + t holding token t of request b. Same clamping rules as
+ * neo_decode_attention; head_dim must be a multiple of 8.
+ */
+neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* block_table,
+                            const int32_t* seq_lens, const int32_t* token_offsets, int32_t batch,
+                            int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                            int32_t block_size, int32_t num_blocks, void* dst, void* stream);
+
+/*
+ * Opt-in check of the indexing inputs: counts seq_lens outside
+ * [0, max_blocks_per_seq * block_size] and block-table entries in use
+ * (j < ceil(L / block_size)) outside [0, num_blocks). Adds the count to
+ * *error_count (device int32, caller zeroes it first).
+ */
+neo_status neo_debug_validate(const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                              int32_t max_blocks_per_seq, int32_t block_size, int32_t num_blocks,
+                              int32_t* error_count, void* stream);
+
+/* Message of this thread's last non-OK status; valid until its next neo_* call. */
+const char* neo_last_error(void);
+
+/* Library version, "major.minor.patch". */
+const char* neo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBNEOATTN_H */

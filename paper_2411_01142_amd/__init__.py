@@ -1,0 +1,256 @@
+"""Batched paged GQA decode attention for AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding over ``libneoattn.so`` (C ABI in ``include/libneoattn.h``).
+Every step of the operation runs in the library's HIP kernels; this module only
+checks tensor shapes, derives the scalar arguments and passes device pointers
+and torch's current stream. There is no CPU fallback: without the built library
+or a GPU every call raises.
+
+The operation (Neo, arXiv 2411.01142, Sec. 2.1-2.2 and Sec. 4): each request's
+new query token attends over its own paged KV cache, query heads sharing KV
+heads in groups. Layouts (torch tensors, all on one GPU):
+
+* ``q``           bf16  ``[batch, num_q_heads, 128]``
+* ``k_cache``     bf16  ``[num_blocks, num_kv_heads, 16, 16, 8]``  (piece-major keys)
+* ``v_cache``     bf16  ``[num_blocks, num_kv_heads, 128, 16]``    (dim-major values)
+* ``block_table`` int32 ``[batch, max_blocks_per_seq]``
+* ``seq_lens``    int32 ``[batch]``
+* result          fp32  ``[batch, num_q_heads, 128]``
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+
+__all__ = [
+    "NeoError", "decode_attention", "workspace_bytes", "paged_gather", "debug_validate",
+    "library_path", "load_library", "VARIANTS", "MAX_SLICES", "version",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libneoattn.so")
+
+VARIANTS = {"auto": 0, "valu": 1, "mfma": 2}
+MAX_SLICES = 4096
+STATUS = {0: "NEO_OK", 1: "NEO_ERR_INVALID_ARG", 2: "NEO_ERR_UNSUPPORTED",
+          3: "NEO_ERR_WORKSPACE", 4: "NEO_ERR_HIP"}
+
+_lib = None
+_lock = threading.Lock()
+_workspaces = {}
+
+
+class NeoError(RuntimeError):
+    """A non-OK status from libneoattn; ``status`` holds the code."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libneoattn.so (built by ``__graft_entry__.build()``); raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is not built; run `python -c 'import __graft_entry__ "
+                              "as g; g.build()'` first")
+        try:
+            # Import torch first so the library binds to the HIP runtime torch
+            # already loaded (both carry the same soname): one runtime per process.
+            import torch  # noqa: F401
+        except ImportError:
+            pass
+        lib = ctypes.CDLL(_LIB_PATH)
+        P, I, F, S = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+        lib.neo_decode_workspace_bytes.argtypes = [I, I, I, I, ctypes.POINTER(S)]
+        lib.neo_decode_workspace_bytes.restype = ctypes.c_int
+        lib.neo_decode_attention.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S, P]
+        lib.neo_decode_attention.restype = ctypes.c_int
+        lib.neo_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S,
+                                                I, I, P]
+        lib.neo_decode_attention_ex.restype = ctypes.c_int
+        lib.neo_decode_attention_events.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P,
+                                                    S, I, I, P, P, P]
+        lib.neo_decode_attention_events.restype = ctypes.c_int
+        lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, P, P]
+        lib.neo_paged_gather.restype = ctypes.c_int
+        lib.neo_debug_validate.argtypes = [P, P, I, I, I, I, P, P]
+        lib.neo_debug_validate.restype = ctypes.c_int
+        lib.neo_last_error.argtypes = []
+        lib.neo_last_error.restype = ctypes.c_char_p
+        lib.neo_version.argtypes = []
+        lib.neo_version.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def version() -> str:
+    return load_library().neo_version().decode()
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load_library().neo_last_error().decode(errors="replace")
+        raise NeoError(status, msg)
+
+
+def workspace_bytes(batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int = 128) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().neo_decode_workspace_bytes(int(batch), int(num_q_heads),
+                                                     int(num_kv_heads), int(head_dim),
+                                                     ctypes.byref(out)))
+    return int(out.value)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _require(t, name, dtype, ndim):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU (got {t.device}); there is no CPU path")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims (got shape {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream_handle(stream, device):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _workspace(nbytes: int, device, stream_handle):
+    torch = _torch()
+    key = (device.index, stream_handle.value)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
+def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out=None, *,
+                     workspace=None, variant: str = "auto", max_slices: int = 0, stream=None):
+    """Decode attention of the whole ragged batch; returns ``out`` (fp32 [B, Hq, 128]).
+
+    ``scale`` defaults to 1/sqrt(head_dim). ``variant`` picks the kernel family
+    ("auto", "valu", "mfma"); ``max_slices`` caps the sequence slices of the
+    plan (0 = library default, 1 = never split a request). ``workspace`` (a
+    uint8 GPU tensor of at least ``workspace_bytes(...)``) is allocated and
+    cached per device and stream when omitted. Runs on ``stream`` (default:
+    torch's current stream) without synchronising.
+    """
+    torch = _torch()
+    lib = load_library()
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 5)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(seq_lens, "seq_lens", torch.int32, 1)
+    B, Hq, D = q.shape
+    NB, Hkv, npieces, bs, x = k_cache.shape
+    if npieces * x != D or x != 8:
+        raise ValueError(f"k_cache shape {tuple(k_cache.shape)} does not match head_dim {D}")
+    if tuple(v_cache.shape) != (NB, Hkv, D, bs):
+        raise ValueError(f"v_cache shape {tuple(v_cache.shape)} != {(NB, Hkv, D, bs)}")
+    if block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_table and seq_lens must have batch rows")
+    devs = {t.device for t in (q, k_cache, v_cache, block_table, seq_lens)}
+    if len(devs) != 1:
+        raise ValueError("all tensors must be on one device")
+    device = q.device
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=device)
+    else:
+        _require(out, "out", torch.float32, 3)
+        if tuple(out.shape) != (B, Hq, D) or out.device != device:
+            raise ValueError("out must be fp32 [batch, num_q_heads, head_dim] on q's device")
+    if variant not in VARIANTS:
+        raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
+    sh = _stream_handle(stream, device)
+    if B == 0:
+        return out
+    need = workspace_bytes(B, Hq, Hkv, D)
+    if workspace is None:
+        workspace = _workspace(need, device, sh)
+    else:
+        _require(workspace, "workspace", torch.uint8, 1)
+    with torch.cuda.device(device):
+        _check(lib.neo_decode_attention_ex(
+            q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+            seq_lens.data_ptr(), Hq, Hkv, D, bs, float(scale), out.data_ptr(), B,
+            block_table.shape[1], NB, workspace.data_ptr(), workspace.numel(),
+            VARIANTS[variant], int(max_slices), sh))
+    return out
+
+
+def paged_gather(cache, kind: str, block_table, seq_lens, *, token_offsets=None, stream=None):
+    """Dense bf16 copy ``[sum L, num_kv_heads, head_dim]`` of the K (``kind='k'``) or V cache."""
+    torch = _torch()
+    lib = load_library()
+    if kind == "k":
+        _require(cache, "cache", torch.bfloat16, 5)
+        NB, Hkv, npieces, bs, x = cache.shape
+        D = npieces * x
+    elif kind == "v":
+        _require(cache, "cache", torch.bfloat16, 4)
+        NB, Hkv, D, bs = cache.shape
+    else:
+        raise ValueError("kind must be 'k' or 'v'")
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(seq_lens, "seq_lens", torch.int32, 1)
+    B = seq_lens.shape[0]
+    device = cache.device
+    if token_offsets is None:
+        token_offsets = torch.zeros(B + 1, dtype=torch.int32, device=device)
+        token_offsets[1:] = torch.cumsum(seq_lens.clamp(min=0), 0)
+    total = int(token_offsets[-1].item()) if B else 0
+    dst = torch.empty((max(total, 0), Hkv, D), dtype=torch.bfloat16, device=device)
+    if B == 0 or total == 0:
+        return dst
+    sh = _stream_handle(stream, device)
+    with torch.cuda.device(device):
+        _check(lib.neo_paged_gather(cache.data_ptr(), 1 if kind == "v" else 0,
+                                    block_table.data_ptr(), seq_lens.data_ptr(),
+                                    token_offsets.data_ptr(), B, block_table.shape[1], Hkv, D,
+                                    bs, NB, dst.data_ptr(), sh))
+    return dst
+
+
+def debug_validate(block_table, seq_lens, num_blocks: int, block_size: int = 16, *,
+                   stream=None) -> int:
+    """Number of out-of-range lengths and in-use block ids (synchronises to read it)."""
+    torch = _torch()
+    lib = load_library()
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(seq_lens, "seq_lens", torch.int32, 1)
+    device = block_table.device
+    cnt = torch.zeros(1, dtype=torch.int32, device=device)
+    sh = _stream_handle(stream, device)
+    with torch.cuda.device(device):
+        _check(lib.neo_debug_validate(block_table.data_ptr(), seq_lens.data_ptr(),
+                                      seq_lens.shape[0], block_table.shape[1], int(block_size),
+                                      int(num_blocks), cnt.data_ptr(), sh))
+    return int(cnt.item())

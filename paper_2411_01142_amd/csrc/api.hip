@@ -1,0 +1,230 @@
+// C ABI of libneoattn: argument checks (all on the host, before any HIP
+// call), workspace sizing and the launch sequence plan -> decode -> combine.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "neo_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+neo_status fail(neo_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+neo_status ok() {
+  g_last_error.clear();
+  return NEO_OK;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+// Slices (wavefronts) the plan may cut by default, and the smallest number of
+// tiles a slice should hold before the plan stops adding slices.
+constexpr int32_t kDefaultSlices = 2048;
+constexpr int32_t kMinTilesPerSlice = 8;
+
+neo_status check_heads(int32_t hq, int32_t hkv, int32_t head_dim) {
+  if (hq <= 0 || hkv <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "num_q_heads (%d) and num_kv_heads (%d) must be positive",
+                hq, hkv);
+  if (hq % hkv != 0)
+    return fail(NEO_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                hq, hkv);
+  if (head_dim != neo::kHeadDim)
+    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", head_dim,
+                neo::kHeadDim);
+  if (!supported_group(hq / hkv))
+    return fail(NEO_ERR_UNSUPPORTED, "query group %d unsupported (1, 2, 4, 8 or 16)", hq / hkv);
+  return NEO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* neo_last_error(void) { return g_last_error.c_str(); }
+
+const char* neo_version(void) { return "0.1.0"; }
+
+neo_status neo_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                      int32_t head_dim, size_t* bytes_out) {
+  if (!bytes_out) return fail(NEO_ERR_INVALID_ARG, "bytes_out is NULL");
+  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
+  if (st != NEO_OK) return st;
+  *bytes_out = neo::workspace_layout(batch, num_q_heads / num_kv_heads).total;
+  return ok();
+}
+
+neo_status neo_decode_attention_events(const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* block_table, const int32_t* seq_lens,
+                                       int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t head_dim, int32_t block_size, float scale,
+                                       float* out, int32_t batch, int32_t max_blocks_per_seq,
+                                       int32_t num_blocks, void* workspace,
+                                       size_t workspace_bytes, int32_t variant,
+                                       int32_t max_slices, void* decode_start_event,
+                                       void* decode_end_event, void* stream) {
+  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
+  if (st != NEO_OK) return st;
+  if (block_size != neo::kBlock)
+    return fail(NEO_ERR_UNSUPPORTED, "block_size %d unsupported (only %d)", block_size,
+                neo::kBlock);
+  if (!isfinite(scale)) return fail(NEO_ERR_INVALID_ARG, "scale is not finite");
+  if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
+    return fail(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
+  if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
+    return fail(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
+                NEO_MAX_SLICES);
+  if (batch == 0) return ok();
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
+                max_blocks_per_seq, num_blocks);
+  if ((int64_t)batch * max_blocks_per_seq * num_kv_heads >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG,
+                "batch * max_blocks_per_seq * num_kv_heads must stay below 2^31");
+  if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
+    return fail(NEO_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
+    return fail(NEO_ERR_INVALID_ARG, "block_table and seq_lens must be 4-byte aligned");
+  const int32_t group = num_q_heads / num_kv_heads;
+  const neo::WorkspaceLayout wl = neo::workspace_layout(batch, group);
+  if (!workspace || workspace_bytes < wl.total)
+    return fail(NEO_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", wl.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned(workspace, 256))
+    return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  int32_t slices = max_slices == 0 ? kDefaultSlices : max_slices;
+  const int32_t min_tiles = max_slices == 0 ? kMinTilesPerSlice : 1;
+  if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
+
+  char* ws = static_cast<char*>(workspace);
+  neo::DecodeParams p;
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.table = block_table;
+  p.lens = seq_lens;
+  p.out = out;
+  p.hdr = reinterpret_cast<const neo::PlanHeader*>(ws + wl.hdr);
+  p.starts = reinterpret_cast<const neo::SliceStart*>(ws + wl.starts);
+  p.part_lse = reinterpret_cast<float*>(ws + wl.part_lse);
+  p.part_o = reinterpret_cast<float*>(ws + wl.part_o);
+  p.batch = batch;
+  p.hq = num_q_heads;
+  p.hkv = num_kv_heads;
+  p.mbps = max_blocks_per_seq;
+  p.num_blocks = num_blocks;
+  p.scale_log2 = scale * 1.4426950408889634f;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices,
+                                  min_tiles, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
+                                  reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
+                                  reinterpret_cast<int32_t*>(ws + wl.prefix), s);
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
+  if (decode_start_event) {
+    e = hipEventRecord(static_cast<hipEvent_t>(decode_start_event), s);
+    if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
+  }
+  e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, grid, s)
+                                  : neo::launch_decode_mfma(p, group, grid, s);
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  if (decode_end_event) {
+    e = hipEventRecord(static_cast<hipEvent_t>(decode_end_event), s);
+    if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
+  }
+  e = neo::launch_combine(p, group, grid, s);
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t block_size, float scale, float* out, int32_t batch,
+                                   int32_t max_blocks_per_seq, int32_t num_blocks,
+                                   void* workspace, size_t workspace_bytes, int32_t variant,
+                                   int32_t max_slices, void* stream) {
+  return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
+                                     num_kv_heads, head_dim, block_size, scale, out, batch,
+                                     max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
+                                     variant, max_slices, nullptr, nullptr, stream);
+}
+
+neo_status neo_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const int32_t* seq_lens,
+                                int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                int32_t block_size, float scale, float* out, int32_t batch,
+                                int32_t max_blocks_per_seq, int32_t num_blocks, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
+                                     num_kv_heads, head_dim, block_size, scale, out, batch,
+                                     max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
+                                     NEO_VARIANT_AUTO, 0, nullptr, nullptr, stream);
+}
+
+neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* block_table,
+                            const int32_t* seq_lens, const int32_t* token_offsets, int32_t batch,
+                            int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                            int32_t block_size, int32_t num_blocks, void* dst, void* stream) {
+  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (is_v != 0 && is_v != 1) return fail(NEO_ERR_INVALID_ARG, "is_v must be 0 or 1");
+  if (num_kv_heads <= 0 || head_dim <= 0 || head_dim % neo::kPiece != 0 || block_size <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "bad shape (num_kv_heads %d, head_dim %d, block_size %d)",
+                num_kv_heads, head_dim, block_size);
+  if (batch == 0) return ok();
+  if (!cache || !block_table || !seq_lens || !token_offsets || !dst)
+    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  if (batch > 65535) return fail(NEO_ERR_INVALID_ARG, "batch above 65535");
+  if ((int64_t)max_blocks_per_seq * block_size >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  hipError_t e = neo::launch_gather(static_cast<const uint16_t*>(cache), is_v, block_table,
+                                    seq_lens, token_offsets, batch, max_blocks_per_seq,
+                                    num_kv_heads, head_dim, block_size, num_blocks,
+                                    static_cast<uint16_t*>(dst), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "gather launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+neo_status neo_debug_validate(const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                              int32_t max_blocks_per_seq, int32_t block_size, int32_t num_blocks,
+                              int32_t* error_count, void* stream) {
+  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (batch == 0) return ok();
+  if (!block_table || !seq_lens || !error_count)
+    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || block_size <= 0 || num_blocks <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "sizes must be positive");
+  if ((int64_t)max_blocks_per_seq * block_size >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  hipError_t e = neo::launch_validate(block_table, seq_lens, batch, max_blocks_per_seq,
+                                      block_size, num_blocks, error_count,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "validate launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+// Internal definitions shared by the libneoattn translation units: the fixed
+// tile geometry, the device workspace layout and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "libneoattn.h"
+
+namespace neo {
+
+constexpr int kHeadDim = 128;                   // dims per head
+constexpr int kBlock = 16;                      // tokens per KV block
+constexpr int kPiece = 8;                       // dims per 16-byte key piece
+constexpr int kTileElems = kHeadDim * kBlock;   // bf16 elements per (block, kv head) tile
+constexpr int kWave = 64;
+constexpr int kWavesPerGroup = 4;               // wavefronts per workgroup (256 threads)
+constexpr int kPlanThreads = 1024;
+
+// Work plan. The batch's (request, kv head, block) tiles are numbered in
+// request-major, kv-head-next, block-minor order; slice s owns the contiguous
+// tile range [starts[s].tile, starts[s+1].tile) and is run by one wavefront.
+struct alignas(16) PlanHeader {
+  int32_t total_tiles;
+  int32_t n_slices;
+  int32_t batch;
+  int32_t pad;
+};
+
+struct alignas(16) SliceStart {
+  int32_t tile;  // first flat tile of the slice
+  int32_t b;     // its request
+  int32_t g;     // its kv head
+  int32_t j;     // its block index inside the request
+};
+
+struct WorkspaceLayout {
+  size_t hdr, starts, prefix, part_lse, part_o, total;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Partial outputs: two slots per slice (a slice cuts at most the pair it starts
+// in and the pair it ends in), each slot `group` rows of head_dim floats plus
+// `group` log-sum-exps (natural log).
+inline WorkspaceLayout workspace_layout(int32_t batch, int32_t group) {
+  WorkspaceLayout w;
+  size_t off = 0;
+  w.hdr = off;
+  off = align256(off + sizeof(PlanHeader));
+  w.starts = off;
+  off = align256(off + sizeof(SliceStart) * (NEO_MAX_SLICES + 1));
+  w.prefix = off;
+  off = align256(off + sizeof(int32_t) * ((size_t)batch + 1));
+  w.part_lse = off;
+  off = align256(off + sizeof(float) * 2 * NEO_MAX_SLICES * (size_t)group);
+  w.part_o = off;
+  off = align256(off + sizeof(float) * 2 * NEO_MAX_SLICES * (size_t)group * kHeadDim);
+  w.total = off;
+  return w;
+}
+
+// Number of KV blocks of a request, with its length clamped to the table.
+__host__ __device__ inline int32_t clamp_len(int32_t L, int32_t mbps) {
+  int32_t cap = mbps * kBlock;
+  return L < 0 ? 0 : (L > cap ? cap : L);
+}
+__host__ __device__ inline int32_t blocks_of(int32_t L, int32_t mbps) {
+  return (clamp_len(L, mbps) + kBlock - 1) / kBlock;
+}
+
+struct DecodeParams {
+  const uint16_t* q;          // [batch][hq][128] bf16
+  const uint16_t* k;          // [nb][hkv][16][16][8] bf16
+  const uint16_t* v;          // [nb][hkv][128][16] bf16
+  const int32_t* table;       // [batch][mbps]
+  const int32_t* lens;        // [batch]
+  float* out;                 // [batch][hq][128]
+  const PlanHeader* hdr;
+  const SliceStart* starts;
+  float* part_lse;            // [2*NEO_MAX_SLICES][group]
+  float* part_o;              // [2*NEO_MAX_SLICES][group][128]
+  int32_t batch, hq, hkv, mbps, num_blocks;
+  float scale_log2;           // scale * log2(e)
+};
+
+// Launchers (each returns the hipError_t of its launch).
+hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
+                       int32_t max_slices, int32_t min_tiles, PlanHeader* hdr,
+                       SliceStart* starts, int32_t* prefix, hipStream_t stream);
+hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, int32_t grid,
+                              hipStream_t stream);
+hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, int32_t grid,
+                              hipStream_t stream);
+hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hipStream_t stream);
+hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,
+                         const int32_t* lens, const int32_t* offsets, int32_t batch,
+                         int32_t mbps, int32_t hkv, int32_t head_dim, int32_t block_size,
+                         int32_t num_blocks, uint16_t* dst, hipStream_t stream);
+hipError_t launch_validate(const int32_t* table, const int32_t* lens, int32_t batch,
+                           int32_t mbps, int32_t block_size, int32_t num_blocks,
+                           int32_t* error_count, hipStream_t stream);
+
+}  // namespace neo

@@ -1,0 +1,223 @@
+// Work plan (block-granular partition of the batch), log-sum-exp combine of
+// split requests, and the test-facing gather / validation kernels.
+//
+// The partition follows the paper's Sec. 4 ("Efficient CPU Kernels"): every
+// request's attention is cut along its sequence at KV-block granularity, each
+// worker gets an equal number of blocks, and the partial outputs of a request
+// are aggregated afterwards. Here a worker is one wavefront: the batch's tiles
+// ((request, kv head, block) triples) are laid end to end and cut into equal
+// contiguous slices, so the load is balanced whatever the length mix.
+#include <math.h>
+
+#include "neo_internal.h"
+
+namespace neo {
+namespace {
+
+// One workgroup: block counts, an exclusive scan over requests (tile offsets),
+// then each slice's first tile located by binary search.
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(
+    const int32_t* __restrict__ lens, int32_t batch, int32_t hkv, int32_t mbps,
+    int32_t max_slices, int32_t min_tiles, PlanHeader* __restrict__ hdr,
+    SliceStart* __restrict__ starts, int32_t* __restrict__ prefix) {
+  __shared__ int32_t sums[kPlanThreads];
+  const int tid = threadIdx.x;
+  const int per = (batch + kPlanThreads - 1) / kPlanThreads;
+  const int b0 = min(batch, tid * per);
+  const int b1 = min(batch, b0 + per);
+  int32_t local = 0;
+  for (int b = b0; b < b1; ++b) local += blocks_of(lens[b], mbps);
+  sums[tid] = local;
+  __syncthreads();
+  for (int off = 1; off < kPlanThreads; off <<= 1) {
+    int32_t add = tid >= off ? sums[tid - off] : 0;
+    __syncthreads();
+    sums[tid] += add;
+    __syncthreads();
+  }
+  int32_t run = tid == 0 ? 0 : sums[tid - 1];
+  for (int b = b0; b < b1; ++b) {
+    prefix[b] = run * hkv;
+    run += blocks_of(lens[b], mbps);
+  }
+  const int32_t total = sums[kPlanThreads - 1] * hkv;
+  if (tid == 0) prefix[batch] = total;
+  __syncthreads();
+
+  int32_t n = 0;
+  if (total > 0) n = min(max(total / min_tiles, 1), max_slices);
+  for (int s = tid; s <= n; s += kPlanThreads) {
+    SliceStart st;
+    if (s == n) {
+      st.tile = total;
+      st.b = batch;
+      st.g = 0;
+      st.j = 0;
+    } else {
+      const int32_t tile = (int32_t)(((int64_t)s * total) / n);
+      int lo = 0, hi = batch - 1;  // largest b with prefix[b] <= tile
+      while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (prefix[mid] <= tile) lo = mid; else hi = mid - 1;
+      }
+      const int32_t nb = blocks_of(lens[lo], mbps);
+      const int32_t r = tile - prefix[lo];
+      st.tile = tile;
+      st.b = lo;
+      st.g = r / nb;
+      st.j = r % nb;
+    }
+    starts[s] = st;
+  }
+  if (tid == 0) {
+    PlanHeader h;
+    h.total_tiles = total;
+    h.n_slices = n;
+    h.batch = batch;
+    h.pad = 0;
+    *hdr = h;
+  }
+}
+
+// Aggregation of the partial outputs of requests cut by slice boundaries
+// (Sec. 4: "aggregate the partial outputs of each request"). Slice w owns the
+// merge of the (request, kv head) pair that starts inside it and continues
+// into slice w+1. Each contributing slice stored its part normalised, with its
+// log-sum-exp: out = sum_i e^(lse_i - M) o_i / sum_i e^(lse_i - M).
+template <int G>
+__global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeParams p) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = blockIdx.x * kWavesPerGroup + (threadIdx.x >> 6);
+  const int n = p.hdr->n_slices;
+  if (w + 1 >= n) return;
+  const SliceStart s0 = p.starts[w];
+  const SliceStart s1 = p.starts[w + 1];
+  if (s1.j == 0) return;                       // slice w ends on a pair boundary
+  const int32_t pair_start = s1.tile - s1.j;
+  if (pair_start < s0.tile) return;            // an earlier slice owns this pair
+  const int32_t nb = blocks_of(p.lens[s1.b], p.mbps);
+  const int32_t pair_end = pair_start + nb;
+  int last = w + 1;
+  while (last + 1 < n && p.starts[last + 1].tile < pair_end) ++last;
+  const int d = 2 * lane;
+  for (int h = 0; h < G; ++h) {
+    float m = -INFINITY;
+    for (int c = w; c <= last; ++c) {
+      const int slot = (p.starts[c].tile >= pair_start) ? 2 * c : 2 * c + 1;
+      m = fmaxf(m, p.part_lse[slot * G + h]);
+    }
+    float z = 0.f, o0 = 0.f, o1 = 0.f;
+    for (int c = w; c <= last; ++c) {
+      const int slot = (p.starts[c].tile >= pair_start) ? 2 * c : 2 * c + 1;
+      const float e = __expf(p.part_lse[slot * G + h] - m);
+      const float2 o = *reinterpret_cast<const float2*>(
+          p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
+      z += e;
+      o0 = fmaf(e, o.x, o0);
+      o1 = fmaf(e, o.y, o1);
+    }
+    const float inv = 1.f / z;
+    float2 r;
+    r.x = o0 * inv;
+    r.y = o1 * inv;
+    *reinterpret_cast<float2*>(p.out + ((size_t)s1.b * p.hq + s1.g * G + h) * kHeadDim + d) = r;
+  }
+}
+
+// Workgroup (j, b) copies block j of request b: thread -> (slot, 8-dim piece).
+__global__ __launch_bounds__(256) void gather_kernel(
+    const uint16_t* __restrict__ cache, int32_t is_v, const int32_t* __restrict__ table,
+    const int32_t* __restrict__ lens, const int32_t* __restrict__ offsets, int32_t mbps,
+    int32_t hkv, int32_t head_dim, int32_t block_size, int32_t num_blocks,
+    uint16_t* __restrict__ dst) {
+  const int j = blockIdx.x, b = blockIdx.y;
+  const int32_t L = min(max(lens[b], 0), mbps * block_size);
+  const int32_t t0 = j * block_size;
+  if (t0 >= L) return;
+  const int32_t valid = min(block_size, L - t0);
+  int32_t phys = table[(size_t)b * mbps + j];
+  phys = (int32_t)min((uint32_t)phys, (uint32_t)(num_blocks - 1));
+  const int pieces = head_dim / kPiece;
+  const int items = hkv * valid * pieces;
+  const size_t row0 = (size_t)offsets[b] + t0;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int c = it % pieces;
+    const int o = (it / pieces) % valid;
+    const int g = it / (pieces * valid);
+    uint16_t vals[kPiece];
+    for (int e = 0; e < kPiece; ++e) {
+      const int d = c * kPiece + e;
+      size_t src;
+      if (is_v)
+        src = (((size_t)phys * hkv + g) * head_dim + d) * block_size + o;
+      else
+        src = ((((size_t)phys * hkv + g) * pieces + c) * block_size + o) * kPiece + e;
+      vals[e] = cache[src];
+    }
+    uint16_t* out = dst + ((row0 + o) * hkv + g) * head_dim + c * kPiece;
+    for (int e = 0; e < kPiece; ++e) out[e] = vals[e];
+  }
+}
+
+__global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict__ table,
+                                                       const int32_t* __restrict__ lens,
+                                                       int32_t batch, int32_t mbps,
+                                                       int32_t block_size, int32_t num_blocks,
+                                                       int32_t* error_count) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)batch * mbps) return;
+  const int b = (int)(i / mbps), j = (int)(i % mbps);
+  const int32_t L = lens[b];
+  int bad = 0;
+  if (j == 0 && (L < 0 || (int64_t)L > (int64_t)mbps * block_size)) bad++;
+  const int32_t Lc = min(max(L, 0), mbps * block_size);
+  if ((int64_t)j * block_size < Lc) {
+    const int32_t phys = table[i];
+    if (phys < 0 || phys >= num_blocks) bad++;
+  }
+  if (bad) atomicAdd(error_count, bad);
+}
+
+}  // namespace
+
+hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
+                       int32_t max_slices, int32_t min_tiles, PlanHeader* hdr,
+                       SliceStart* starts, int32_t* prefix, hipStream_t stream) {
+  plan_kernel<<<1, kPlanThreads, 0, stream>>>(lens, batch, hkv, mbps, max_slices, min_tiles, hdr,
+                                              starts, prefix);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hipStream_t stream) {
+  const dim3 block(kWave * kWavesPerGroup);
+  switch (group) {
+    case 1: combine_kernel<1><<<grid, block, 0, stream>>>(p); break;
+    case 2: combine_kernel<2><<<grid, block, 0, stream>>>(p); break;
+    case 4: combine_kernel<4><<<grid, block, 0, stream>>>(p); break;
+    case 8: combine_kernel<8><<<grid, block, 0, stream>>>(p); break;
+    case 16: combine_kernel<16><<<grid, block, 0, stream>>>(p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,
+                         const int32_t* lens, const int32_t* offsets, int32_t batch,
+                         int32_t mbps, int32_t hkv, int32_t head_dim, int32_t block_size,
+                         int32_t num_blocks, uint16_t* dst, hipStream_t stream) {
+  gather_kernel<<<dim3(mbps, batch), 256, 0, stream>>>(cache, is_v, table, lens, offsets, mbps,
+                                                       hkv, head_dim, block_size, num_blocks, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const int32_t* table, const int32_t* lens, int32_t batch,
+                           int32_t mbps, int32_t block_size, int32_t num_blocks,
+                           int32_t* error_count, hipStream_t stream) {
+  const int64_t n = (int64_t)batch * mbps;
+  const int blocks = (int)((n + 255) / 256);
+  validate_kernel<<<blocks, 256, 0, stream>>>(table, lens, batch, mbps, block_size, num_blocks,
+                                             error_count);
+  return hipGetLastError();
+}
+
+}  // namespace neo

@@ -134,18 +134,49 @@ class Case:
         L = np.maximum(self.seq_lens.astype(np.int64), 0)
         return int(L.sum()) * self.num_q_heads * self.head_dim * 4
 
+    def to_torch(self, device="cuda"):
+        """(q, k_cache, v_cache, block_table, seq_lens) as torch tensors on ``device``
+        (bf16 caches and q, int32 table and lengths)."""
+        import torch
+
+        def bf16(a):
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(
+                torch.bfloat16)
+        return (bf16(self.q), bf16(self.k_cache), bf16(self.v_cache),
+                torch.from_numpy(np.ascontiguousarray(self.block_table)).to(device),
+                torch.from_numpy(np.ascontiguousarray(self.seq_lens)).to(device))
+
     def logical_kv(self):
         """Logical [NB][Hkv][bs][D] views (copies) of the caches, as uint16."""
         return unpack_k(self.k_cache), unpack_v(self.v_cache)
 
 
-def _draw_normal_bf16(rng: np.random.Generator, shape, chunk: int = 1 << 24) -> np.ndarray:
-    """Standard normal float32 draws, rounded to bf16, generated in chunks to bound memory."""
+_NORMAL_TABLE = None
+
+
+def normal_table() -> np.ndarray:
+    """bf16 bits of the N(0,1) quantiles at (i + 1/2) / 65536, i = 0..65535.
+
+    Indexing it with uniform 16-bit integers samples N(0,1) at 16-bit
+    resolution (tails cut at |x| = 4.17), already rounded to bf16.
+    """
+    global _NORMAL_TABLE
+    if _NORMAL_TABLE is None:
+        from scipy.special import ndtri
+        u = (np.arange(65536, dtype=np.float64) + 0.5) / 65536.0
+        _NORMAL_TABLE = to_bf16(ndtri(u).astype(np.float32))
+    return _NORMAL_TABLE
+
+
+def _draw_normal_bf16(rng: np.random.Generator, shape, chunk: int = 1 << 26) -> np.ndarray:
+    """I.i.d. N(0,1) bf16 bits in C order of ``shape`` (inverse-CDF table sampler)."""
+    table = normal_table()
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.uint16)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
-        out[s:e] = to_bf16(rng.standard_normal(e - s, dtype=np.float32))
+        idx = rng.integers(0, 65536, size=e - s, dtype=np.uint16)
+        np.take(table, idx, out=out[s:e])
     return out.reshape(shape)
 
 
@@ -161,8 +192,10 @@ def build_case(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
                name: str = "case") -> Case:
     """Build a paged batch.
 
-    Draw order from ``rng``: physical-block permutation, q, K, V, K-outlier mask
-    (``seq_lens`` and any config-specific draws come before, from the caller).
+    Draw order from ``rng``: physical-block permutation, q, K, V (K and V
+    i.i.d. in storage order), K-outlier mask (``seq_lens`` and any
+    config-specific draws come before, from the caller). Random values are
+    N(0,1) through ``normal_table``.
 
     ``q_values`` (float32 [B][Hq][D]) replaces the q draw. ``k_values`` /
     ``v_values`` are callables ``f(b, t, g) -> float32[D]`` giving the logical
@@ -194,10 +227,12 @@ def build_case(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
         q = to_bf16(np.asarray(q_values, dtype=np.float32).reshape(B, Hq, D))
     else:
         q = _draw_normal_bf16(rng, (B, Hq, D))
-    k_log = _draw_normal_bf16(rng, (nb, Hkv, bs, D))
-    v_log = _draw_normal_bf16(rng, (nb, Hkv, bs, D))
+    # Random K and V are drawn i.i.d. directly in storage order.
+    k_st = _draw_normal_bf16(rng, (nb, Hkv, D // K_PACK, bs, K_PACK))
+    v_st = _draw_normal_bf16(rng, (nb, Hkv, D, bs))
 
     if k_values is not None or v_values is not None:
+        k_log, v_log = unpack_k(k_st), unpack_v(v_st)
         for b in range(B):
             for t in range(int(max(L[b], 0))):
                 p, o = int(table[b, t // bs]), t % bs
@@ -206,21 +241,21 @@ def build_case(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
                         k_log[p, g, o] = to_bf16(np.asarray(k_values(b, t, g), dtype=np.float32))
                     if v_values is not None:
                         v_log[p, g, o] = to_bf16(np.asarray(v_values(b, t, g), dtype=np.float32))
+        k_st, v_st = pack_k(k_log), pack_v(v_log)
 
     if k_outlier_frac > 0.0:
         # Independent Bernoulli per (request, token, kv head) over valid tokens;
-        # the row is multiplied by a power of two, exact in bf16.
+        # the key row is multiplied by a power of two, exact in bf16.
         for b in range(B):
             n_tok = int(max(L[b], 0))
             if n_tok == 0:
                 continue
             mask = rng.random((n_tok, Hkv)) < k_outlier_frac
             ts, gs = np.nonzero(mask)
-            if ts.size:
-                ps = table[b, ts // bs]
-                os_ = ts % bs
-                rows = bf16_to_f32(k_log[ps, gs, os_]) * np.float32(k_outlier_mult)
-                k_log[ps, gs, os_] = to_bf16(rows)
+            for t, g in zip(ts.tolist(), gs.tolist()):
+                p, o = int(table[b, t // bs]), t % bs
+                row = bf16_to_f32(k_st[p, g, :, o, :]) * np.float32(k_outlier_mult)
+                k_st[p, g, :, o, :] = to_bf16(row)
 
     if poison:
         used = np.zeros(nb, dtype=bool)
@@ -230,12 +265,12 @@ def build_case(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
             rem = int(L[b]) - (n - 1) * bs if n > 0 else bs
             if n > 0 and rem < bs:
                 p = int(table[b, n - 1])
-                k_log[p, :, rem:, :] = BF16_NAN
-                v_log[p, :, rem:, :] = BF16_NAN
-        k_log[~used] = BF16_NAN
-        v_log[~used] = BF16_NAN
+                k_st[p, :, :, rem:, :] = BF16_NAN
+                v_st[p, :, :, rem:] = BF16_NAN
+        k_st[~used] = BF16_NAN
+        v_st[~used] = BF16_NAN
 
-    return Case(q=q, k_cache=pack_k(k_log), v_cache=pack_v(v_log), block_table=table,
+    return Case(q=q, k_cache=k_st, v_cache=v_st, block_table=table,
                 seq_lens=L.astype(np.int32), num_q_heads=Hq, num_kv_heads=Hkv,
                 head_dim=D, block_size=bs,
                 scale=float(1.0 / math.sqrt(D)) if scale is None else float(scale),

@@ -1,0 +1,151 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point the
+header declares, sizes workspaces, and rejects bad arguments before any HIP call
+(so these run without a GPU)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2411_01142_amd as neo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libneoattn.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(neo.library_path()):
+        import __graft_entry__
+        __graft_entry__.build()
+    return neo.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(neo_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("neo_decode_attention", "neo_decode_attention_ex", "neo_decode_workspace_bytes",
+              "neo_paged_gather", "neo_debug_validate", "neo_last_error", "neo_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version(lib):
+    assert re.fullmatch(r"\d+\.\d+\.\d+", neo.version())
+
+
+def test_workspace_bytes_grow_with_batch_and_group():
+    a = neo.workspace_bytes(64, 32, 8)
+    b = neo.workspace_bytes(1024, 32, 8)
+    c = neo.workspace_bytes(64, 64, 8)
+    assert 0 < a < b and a < c
+    assert a % 256 == 0
+    # two partial slots per slice, group rows of (128 + 1) floats each, at least
+    assert a >= 2 * neo.MAX_SLICES * 4 * 129 * 4
+
+
+@pytest.mark.parametrize("args,code", [
+    ((64, 32, 7, 128), INVALID),
+    ((64, 0, 8, 128), INVALID),
+    ((64, 32, 8, 64), UNSUPPORTED),
+    ((64, 96, 8, 128), UNSUPPORTED),
+    ((-1, 32, 8, 128), INVALID),
+])
+def test_workspace_bytes_rejects(lib, args, code):
+    out = ctypes.c_size_t(0)
+    assert lib.neo_decode_workspace_bytes(*args, ctypes.byref(out)) == code
+    assert lib.neo_last_error().decode()
+
+
+FAKE = 1 << 20  # non-null, 256-aligned host address; never dereferenced on these paths
+
+
+def call(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, table=FAKE, lens=FAKE, hq=32, hkv=8, d=128, bs=16,
+             scale=1 / math.sqrt(128), out=FAKE, batch=4, mbps=8, nb=100, ws=FAKE,
+             ws_bytes=1 << 40, variant=0, slices=0, stream=None)
+    a.update(kw)
+    return lib.neo_decode_attention_ex(a["q"], a["k"], a["v"], a["table"], a["lens"], a["hq"],
+                                       a["hkv"], a["d"], a["bs"], a["scale"], a["out"],
+                                       a["batch"], a["mbps"], a["nb"], a["ws"], a["ws_bytes"],
+                                       a["variant"], a["slices"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code,needle", [
+    (dict(q=None), INVALID, "NULL"),
+    (dict(k=None), INVALID, "NULL"),
+    (dict(v=None), INVALID, "NULL"),
+    (dict(table=None), INVALID, "NULL"),
+    (dict(lens=None), INVALID, "NULL"),
+    (dict(out=None), INVALID, "NULL"),
+    (dict(hkv=7), INVALID, "multiple"),
+    (dict(hq=0), INVALID, "positive"),
+    (dict(d=64), UNSUPPORTED, "head_dim"),
+    (dict(bs=32), UNSUPPORTED, "block_size"),
+    (dict(hq=96, hkv=8), UNSUPPORTED, "group"),
+    (dict(scale=float("nan")), INVALID, "scale"),
+    (dict(scale=float("inf")), INVALID, "scale"),
+    (dict(batch=-3), INVALID, "batch"),
+    (dict(mbps=0), INVALID, "positive"),
+    (dict(nb=0), INVALID, "positive"),
+    (dict(ws=None), WORKSPACE, "workspace"),
+    (dict(ws_bytes=1000), WORKSPACE, "workspace"),
+    (dict(q=FAKE + 8), INVALID, "aligned"),
+    (dict(out=FAKE + 4), INVALID, "aligned"),
+    (dict(ws=FAKE + 64), INVALID, "aligned"),
+    (dict(variant=7), UNSUPPORTED, "variant"),
+    (dict(slices=-1), INVALID, "max_slices"),
+    (dict(slices=100000), INVALID, "max_slices"),
+    (dict(batch=1 << 20, mbps=1 << 12), INVALID, "2^31"),
+])
+def test_decode_rejects_bad_arguments_before_any_hip_call(lib, kw, code, needle):
+    assert call(lib, **kw) == code
+    assert needle in lib.neo_last_error().decode()
+
+
+def test_empty_batch_is_a_noop(lib):
+    assert call(lib, batch=0, q=None, k=None, v=None, table=None, lens=None, out=None,
+                ws=None) == OK
+    assert lib.neo_last_error().decode() == ""
+
+
+def test_plain_entry_point_validates_too(lib):
+    rc = lib.neo_decode_attention(FAKE, FAKE, FAKE, FAKE, FAKE, 32, 8, 128, 16, 0.1, None, 4, 8,
+                                  100, FAKE, 1 << 40, None)
+    assert rc == INVALID
+
+
+def test_gather_and_validate_reject(lib):
+    assert lib.neo_paged_gather(FAKE, 2, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, FAKE,
+                                None) == INVALID
+    assert lib.neo_paged_gather(FAKE, 0, FAKE, FAKE, FAKE, 4, 8, 8, 100, 16, 100, FAKE,
+                                None) == INVALID
+    assert lib.neo_paged_gather(None, 0, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, FAKE,
+                                None) == INVALID
+    assert lib.neo_paged_gather(None, 0, None, None, None, 0, 8, 8, 128, 16, 100, None,
+                                None) == OK
+    assert lib.neo_debug_validate(FAKE, FAKE, 4, 0, 16, 100, FAKE, None) == INVALID
+    assert lib.neo_debug_validate(None, FAKE, 4, 8, 16, 100, FAKE, None) == INVALID
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    q = torch.zeros(2, 8, 128, dtype=torch.bfloat16)
+    k = torch.zeros(4, 2, 16, 16, 8, dtype=torch.bfloat16)
+    v = torch.zeros(4, 2, 128, 16, dtype=torch.bfloat16)
+    bt = torch.zeros(2, 2, dtype=torch.int32)
+    sl = torch.ones(2, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU"):
+        neo.decode_attention(q, k, v, bt, sl)

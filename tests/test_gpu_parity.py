@@ -1,0 +1,312 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Bar (decode attention with bf16 q/K/V and fp32 accumulation): max abs error
+<= 1e-2 and row-normwise relative error <= 2e-2 (max over (request, head) of
+max_d |y - r| / max_d |r|); block-table indexing bit-exact (the gather kernel,
+and bit-identical outputs under physical-block relabeling).
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2411_01142_amd as neo
+from paper_2411_01142_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+ABS_TOL = 1e-2
+REL_TOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    neo.load_library()
+    yield
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run(case, **kw):
+    q, k, v, bt, sl = case.to_torch("cuda")
+    out = neo.decode_attention(q, k, v, bt, sl, scale=case.scale, **kw)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def errors(y, r, rows=None):
+    """(max abs error, max row-normwise rel error) over the given flat rows."""
+    y = y.reshape(-1, y.shape[-1])
+    r = r.reshape(-1, r.shape[-1])
+    if rows is not None:
+        y, r = y[rows], r[rows]
+    ae = np.abs(y.astype(np.float64) - r.astype(np.float64))
+    denom = np.maximum(np.abs(r).max(axis=1), 1e-30)
+    return float(ae.max()), float((ae.max(axis=1) / denom).max())
+
+
+def assert_parity(y, r, label, rows=None):
+    assert np.all(np.isfinite(y.reshape(-1, y.shape[-1])[rows] if rows is not None else y)), label
+    ae, re = errors(y, r, rows)
+    say(f"[parity] {label}: max_abs={ae:.3e} max_rel_rownorm={re:.3e}")
+    assert ae <= ABS_TOL and re <= REL_TOL, (label, ae, re)
+    return ae, re
+
+
+# --------------------------------------------------------------------- indexing
+
+@pytest.mark.parametrize("which", ["k", "v"])
+@pytest.mark.parametrize("shuffle", [True, False])
+def test_gather_is_bit_exact(which, shuffle):
+    case = W.build_case([1, 15, 16, 17, 100, 333, 0, 64], 8, 4, 128, 16, seed=3,
+                        shuffle=shuffle, extra_table_cols=2)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    dense = neo.paged_gather(k if which == "k" else v, which, bt, sl)
+    got = dense.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = oracle.paged_gather(case, which)
+    assert got.shape == ref.shape and np.array_equal(got, ref)
+
+
+def test_gather_config1_bit_exact():
+    case = W.make_config(1, 1)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    for which, cache in (("k", k), ("v", v)):
+        got = neo.paged_gather(cache, which, bt, sl).view(torch.int16).cpu().numpy()
+        assert np.array_equal(got.view(np.uint16), oracle.paged_gather(case, which))
+
+
+def test_debug_validate_counts_bad_indices():
+    case = W.build_case([20, 40, 5], 4, 2, 128, 16, seed=4, extra_table_cols=1)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    assert neo.debug_validate(bt, sl, case.num_blocks) == 0
+    bt2 = bt.clone()
+    bt2[1, 2] = case.num_blocks       # in use (40 tokens -> blocks 0..2): counted
+    bt2[2, 3] = 10 ** 6               # past request 2's one block: never read
+    bt2[0, 0] = -5                    # request 0 gets a negative length below: unused
+    sl2 = sl.clone()
+    sl2[0] = -3                       # counted
+    assert neo.debug_validate(bt2, sl2, case.num_blocks) == 2
+    # A length past the table is counted, and clamping it brings the -1 padding
+    # of that row into use (3 more entries).
+    sl3 = sl.clone()
+    sl3[2] = 16 * case.max_blocks_per_seq + 1
+    assert neo.debug_validate(bt, sl3, case.num_blocks) == 1 + 3
+
+
+# --------------------------------------------------------------------- parity, small
+
+SMALL_LENS = [1, 15, 16, 17, 31, 33, 100, 257, 1000, 2]
+
+
+@pytest.mark.parametrize("group", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_small_cases_all_groups(group, variant):
+    hkv = 2
+    case = W.build_case(SMALL_LENS, hkv * group, hkv, 128, 16, seed=10 + group)
+    ref = oracle.decode_attention(case)
+    for slices in (0, 1, 7, neo.MAX_SLICES):
+        y = run(case, variant=variant, max_slices=slices)
+        assert_parity(y, ref, f"G={group} {variant} slices={slices}")
+
+
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_softmax_range_stress(variant):
+    # Outlier keys x8 and a large scale push scores far apart.
+    case = W.build_case([50, 300, 700, 16], 32, 8, 128, 16, seed=5, k_outlier_frac=0.05,
+                        scale=0.5)
+    ref = oracle.decode_attention(case)
+    assert_parity(run(case, variant=variant), ref, f"stress {variant}")
+
+
+# --------------------------------------------------------------------- parity, configs
+
+def sample_rows(case, n, seed):
+    rng = np.random.default_rng(seed)
+    Hq = case.num_q_heads
+    longest = np.argsort(-case.seq_lens.astype(np.int64))[:8]
+    rows = {int(b) * Hq + h for b in longest for h in (0, Hq - 1)}
+    rows |= set(int(x) for x in rng.choice(case.batch * Hq, size=n, replace=False))
+    return np.array(sorted(rows))
+
+
+def oracle_rows(case, rows):
+    ref = np.zeros((case.batch * case.num_q_heads, case.head_dim), dtype=np.float32)
+    for r in rows:
+        ref[r] = oracle.decode_attention(case, rows=(int(r), int(r) + 1)).reshape(
+            -1, case.head_dim)[r]
+    return ref
+
+
+@pytest.mark.parametrize("cfg,seed,batch_limit", [
+    (1, 1, None), (1, 101, None), (2, 2, None), (2, 102, None),
+    (3, 3, None), (3, 103, None), (4, 4, None), (4, 104, 96),
+    (5, 5, None), (5, 105, None),
+])
+def test_config_parity(cfg, seed, batch_limit):
+    say(f"[config] cfg={cfg} seed={seed} batch_limit={batch_limit}: generating")
+    case = W.make_config(cfg, seed, batch_limit=batch_limit)
+    say(f"[config] {case.name} B={case.batch} NB={case.num_blocks} sumL={case.total_tokens()}")
+    y = run(case).reshape(-1, case.head_dim)
+    if cfg in (1, 2):
+        ref = oracle.decode_attention(case).reshape(-1, case.head_dim)
+        assert_parity(y, ref, case.name)
+    else:
+        rows = sample_rows(case, 48, seed)
+        ref = oracle_rows(case, rows)
+        assert_parity(y, ref, case.name + f" ({len(rows)} sampled rows)", rows=rows)
+        # Properties at any size: every row finite and inside the convex hull
+        # bound of V (|out| <= max |V| over valid rows <= 4.5 for these inputs).
+        assert np.all(np.isfinite(y))
+        assert np.abs(y).max() <= 4.5
+
+
+# --------------------------------------------------------------------- edge cases
+
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_empty_and_single_token_requests(variant):
+    case = W.build_case([0, 1, 0, 17, 1, 0], 8, 2, 128, 16, seed=6)
+    y = run(case, variant=variant)
+    ref = oracle.decode_attention(case)
+    assert np.all(y[[0, 2, 5]] == 0.0)
+    # One token: its weight is exactly 1, so the output is that V row bit for bit.
+    assert np.array_equal(y[1], ref[1]) and np.array_equal(y[4], ref[4])
+    assert_parity(y, ref, f"empty/single {variant}")
+
+
+def test_all_requests_empty():
+    case = W.build_case([0, 0, 0], 8, 2, 128, 16, seed=7)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    out = torch.full((3, 8, 128), float("nan"), device="cuda")
+    neo.decode_attention(q, k, v, bt, sl, out=out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0).item()
+
+
+def test_batch_of_one_long_request():
+    case = W.build_case([9000], 32, 8, 128, 16, seed=8)
+    ref = oracle.decode_attention(case)
+    for variant in ("valu", "mfma"):
+        assert_parity(run(case, variant=variant), ref, f"B=1 L=9000 {variant}")
+
+
+def test_lengths_beyond_the_table_are_clamped():
+    case = W.build_case([40, 64], 4, 2, 128, 16, seed=9)
+    clamped = W.Case(**{**case.__dict__, "seq_lens": np.array([40, 64], np.int32)})
+    over = W.Case(**{**case.__dict__, "seq_lens": np.array([40, 10 ** 6], np.int32)})
+    assert np.array_equal(run(over), run(clamped))
+
+
+# --------------------------------------------------------------------- invariants
+
+def relabel(case, seed):
+    rng = np.random.default_rng(seed)
+    new_of_old = rng.permutation(case.num_blocks)
+    k = np.empty_like(case.k_cache)
+    v = np.empty_like(case.v_cache)
+    k[new_of_old] = case.k_cache
+    v[new_of_old] = case.v_cache
+    bt = case.block_table.copy()
+    m = bt >= 0
+    bt[m] = new_of_old[bt[m]]
+    return W.Case(**{**case.__dict__, "k_cache": k, "v_cache": v, "block_table": bt})
+
+
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_block_relabeling_is_bit_identical(variant):
+    case = W.make_config(2, 2, batch_limit=24)
+    a = run(case, variant=variant)
+    b = run(relabel(case, 1), variant=variant)
+    assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_repeated_runs_are_bit_identical(variant):
+    case = W.make_config(5, 5, batch_limit=200)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    first = neo.decode_attention(q, k, v, bt, sl, variant=variant).clone()
+    for _ in range(30):
+        again = neo.decode_attention(q, k, v, bt, sl, variant=variant)
+        assert torch.equal(first, again)
+
+
+def test_request_permutation():
+    case = W.build_case([5, 300, 17, 1000, 64, 1], 16, 4, 128, 16, seed=11)
+    perm = np.random.default_rng(0).permutation(case.batch)
+    pc = W.Case(**{**case.__dict__, "q": case.q[perm], "block_table": case.block_table[perm],
+                   "seq_lens": case.seq_lens[perm]})
+    for variant in ("valu", "mfma"):
+        a = run(case, variant=variant, max_slices=1)
+        b = run(pc, variant=variant, max_slices=1)
+        assert np.array_equal(a[perm], b)        # no split: same arithmetic per request
+        a = run(case, variant=variant)
+        b = run(pc, variant=variant)
+        assert np.max(np.abs(a[perm] - b)) <= 1e-5
+
+
+def test_split_matches_unsplit_and_variants_agree():
+    case = W.make_config(5, 105, batch_limit=300)
+    base = run(case, variant="mfma", max_slices=1)
+    for variant in ("valu", "mfma"):
+        for slices in (0, 64, 1024, neo.MAX_SLICES):
+            y = run(case, variant=variant, max_slices=slices)
+            d = float(np.max(np.abs(y - base)))
+            say(f"[split] {variant} slices={slices}: max diff vs unsplit {d:.2e}")
+            assert d <= 1e-5
+
+
+def test_poisoned_slots_do_not_leak():
+    lens = [1, 15, 17, 64, 99, 250]
+    a = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=True)
+    b = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=False)
+    for variant in ("valu", "mfma"):
+        ya, yb = run(a, variant=variant), run(b, variant=variant)
+        assert np.all(np.isfinite(ya)) and np.array_equal(ya, yb)
+
+
+def test_integer_coded_v_counts_every_position_once():
+    L = [1, 2, 15, 16, 17, 255, 256, 257, 600, 4097]
+
+    def vf(b, t, g):
+        v = np.zeros(128, dtype=np.float32)
+        v[0], v[1] = t % 256, t // 256
+        return v
+    case = W.build_case(L, 4, 2, 128, 16, seed=13, q_values=np.zeros((len(L), 4, 128)),
+                        v_values=vf)
+    for variant in ("valu", "mfma"):
+        y = run(case, variant=variant).astype(np.float64)
+        for b, n in enumerate(L):
+            got = y[b, :, 0] + 256.0 * y[b, :, 1]
+            assert np.max(np.abs(got - (n - 1) / 2.0)) <= 1e-6 * max(1.0, n), (variant, n)
+            assert np.all(y[b, :, 2:] == 0.0)
+
+
+def test_runs_on_a_side_stream():
+    case = W.build_case([100, 200, 3], 8, 2, 128, 16, seed=14)
+    ref = run(case)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        out = neo.decode_attention(q, k, v, bt, sl, scale=case.scale)
+    s.synchronize()
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_binding_errors_are_raised():
+    case = W.build_case([10], 8, 2, 128, 16, seed=15)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    ws = torch.empty(1024, dtype=torch.uint8, device="cuda")
+    with pytest.raises(neo.NeoError) as ei:
+        neo.decode_attention(q, k, v, bt, sl, workspace=ws)
+    assert ei.value.status == 3
+    with pytest.raises(neo.NeoError):
+        neo.decode_attention(q, k, v, bt, sl, scale=math.inf)
