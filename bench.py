@@ -44,7 +44,8 @@ def log(msg):
 def kernel_source_sha(variant: str) -> str:
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        if name.startswith("decode_") and variant not in name and name != "decode_common.h":
+        if name.startswith("decode_") and name != "decode_common.h" and \
+                name != f"decode_{variant.split('_')[0]}.hip":
             continue
         with open(os.path.join(ROOT, "paper_2411_01142_amd", "csrc", name), "rb") as f:
             h.update(f.read())
@@ -132,6 +133,7 @@ def main(argv=None):
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--variant", default="auto", choices=["auto", "valu", "mfma"])
+    ap.add_argument("--schedule", default="auto", choices=["auto", "fused", "staged"])
     ap.add_argument("--max-slices", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -161,12 +163,13 @@ def main(argv=None):
     reps = [(k, v)] + [(k.clone(), v.clone()) for _ in range(nrep - 1)]
     out = torch.empty((case.batch, case.num_q_heads, case.head_dim), dtype=torch.float32,
                       device="cuda")
-    ws = torch.empty(neo.workspace_bytes(case.batch, case.num_q_heads, case.num_kv_heads),
-                     dtype=torch.uint8, device="cuda")
+    ws = neo.new_workspace(case.batch, case.num_q_heads, case.num_kv_heads)
     lib = neo.load_library()
     stream = torch.cuda.current_stream()
     sh = ctypes.c_void_p(stream.cuda_stream)
     variant_id = neo.VARIANTS[args.variant]
+    schedule_id = neo.SCHEDULES[args.schedule]
+    schedule = "staged" if args.schedule == "staged" else "fused"
     resolved = "mfma" if args.variant == "auto" else args.variant
     hip = HipEvents()
     ev = [(hip.create(), hip.create()) for _ in range(args.steps)]
@@ -177,8 +180,8 @@ def main(argv=None):
             q.data_ptr(), kk.data_ptr(), vv.data_ptr(), bt.data_ptr(), sl.data_ptr(),
             case.num_q_heads, case.num_kv_heads, case.head_dim, case.block_size,
             float(case.scale), out.data_ptr(), case.batch, case.max_blocks_per_seq,
-            case.num_blocks, ws.data_ptr(), ws.numel(), variant_id, args.max_slices,
-            evs[0], evs[1], sh)
+            case.num_blocks, ws.data_ptr(), ws.numel(), variant_id, schedule_id,
+            args.max_slices, evs[0], evs[1], sh)
         if rc != 0:
             raise neo.NeoError(rc, lib.neo_last_error().decode())
 
@@ -203,7 +206,7 @@ def main(argv=None):
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
     dec_ms = sum(decode_ms) / len(decode_ms)
     achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
-    traffic = load_traffic(workload_key, resolved)
+    traffic = load_traffic(workload_key, f"{resolved}_{schedule}")
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -228,12 +231,12 @@ def main(argv=None):
             "num_kv_heads": case.num_kv_heads, "head_dim": case.head_dim,
             "block_size": case.block_size, "sum_seq_len": case.total_tokens(),
             "algorithmic_bytes_per_step": alg_bytes, "kv_replicas": nrep,
-            "variant": resolved, "max_slices": args.max_slices,
+            "variant": resolved, "schedule": schedule, "max_slices": args.max_slices,
             "parallelism": "single GPU",
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": f"decode_{resolved}_kernel<{case.group}>",
+            "kernel": f"decode_{resolved}_kernel<{case.group}, {schedule == 'fused'}>",
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

@@ -77,24 +77,40 @@ typedef enum {
   NEO_VARIANT_MFMA = 2  /* q.K and p.V on bf16 matrix cores, query group padded to 16 */
 } neo_variant;
 
+/* How the call is launched (neo_decode_attention_ex). */
+typedef enum {
+  NEO_SCHEDULE_AUTO = 0,   /* fused */
+  NEO_SCHEDULE_FUSED = 1,  /* one kernel: each wavefront plans its own slice from seq_lens and
+                              the last slice to finish a split request merges it */
+  NEO_SCHEDULE_STAGED = 2  /* three kernels: plan, decode, log-sum-exp combine */
+} neo_schedule;
+
 /* Largest number of sequence slices (one wavefront each) a call may use. */
 #define NEO_MAX_SLICES 4096
 
 /*
  * Bytes of device workspace neo_decode_attention needs: the work plan (slice
  * starts, per-request tile offsets) and room for two partial outputs per slice
- * (group * head_dim fp32 values plus group log-sum-exps each). Depends only on
- * host scalars, so it can be allocated ahead of time. Sized for NEO_MAX_SLICES.
+ * (group * head_dim fp32 values plus group log-sum-exps each), and the arrival
+ * counters of split requests. Depends only on host scalars, so it can be
+ * allocated ahead of time. Sized for NEO_MAX_SLICES.
+ *
+ * The workspace must be zero-filled once before its first use
+ * (neo_decode_workspace_init or any fill); every call leaves its counters at
+ * zero again. Calls that may overlap on the device need distinct workspaces.
  */
 neo_status neo_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                       int32_t head_dim, size_t* bytes_out);
+
+/* Zero-fill a workspace on `stream` with a fill kernel (no memset node). */
+neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Decode attention of the whole ragged batch (the operation and layouts above).
  * The first eleven arguments follow the problem statement in that order; the rest
  * are what a device pointer cannot carry: batch size, block-table row stride
  * (max_blocks_per_seq), pool size (num_blocks), the workspace and the stream.
- * Enqueues three kernels (plan, decode, combine). Reads q, k_cache, v_cache,
+ * Enqueues one kernel (the fused schedule). Reads q, k_cache, v_cache,
  * block_table and seq_lens; writes out and the workspace.
  * batch == 0 is a no-op (pointers may then be NULL).
  */
@@ -106,11 +122,12 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
                                 size_t workspace_bytes, void* stream);
 
 /*
- * As neo_decode_attention, with the kernel family and the number of sequence
- * slices chosen by the caller. max_slices = 0 picks the library default; any
- * value in [1, NEO_MAX_SLICES] caps the number of slices the plan may cut
- * (1 = no request is ever split). The result is the same operation for every
- * choice, up to fp32 summation order.
+ * As neo_decode_attention, with the kernel family (neo_variant), the launch
+ * schedule (neo_schedule) and the number of sequence slices chosen by the
+ * caller. max_slices = 0 picks the library default; any value in
+ * [1, NEO_MAX_SLICES] caps the number of slices the plan may cut (1 = no
+ * request is ever split). The result is the same operation for every choice,
+ * up to fp32 summation order.
  */
 neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* seq_lens,
@@ -118,13 +135,13 @@ neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const voi
                                    int32_t block_size, float scale, float* out, int32_t batch,
                                    int32_t max_blocks_per_seq, int32_t num_blocks,
                                    void* workspace, size_t workspace_bytes, int32_t variant,
-                                   int32_t max_slices, void* stream);
+                                   int32_t schedule, int32_t max_slices, void* stream);
 
 /*
  * As neo_decode_attention_ex, also recording two caller-created HIP events
  * (hipEvent_t, may be NULL) on `stream` immediately before and after the decode
  * kernel, so the main kernel can be timed apart from the plan and combine
- * launches. Meant for measurement.
+ * launches of the staged schedule. Meant for measurement.
  */
 neo_status neo_decode_attention_events(const void* q, const void* k_cache, const void* v_cache,
                                        const int32_t* block_table, const int32_t* seq_lens,
@@ -133,8 +150,9 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        float* out, int32_t batch, int32_t max_blocks_per_seq,
                                        int32_t num_blocks, void* workspace,
                                        size_t workspace_bytes, int32_t variant,
-                                       int32_t max_slices, void* decode_start_event,
-                                       void* decode_end_event, void* stream);
+                                       int32_t schedule, int32_t max_slices,
+                                       void* decode_start_event, void* decode_end_event,
+                                       void* stream);
 
 /*
  * Bit-exact dense copy of one paged cache through the block table (the paged

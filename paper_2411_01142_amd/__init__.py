@@ -26,13 +26,15 @@ import threading
 
 __all__ = [
     "NeoError", "decode_attention", "workspace_bytes", "paged_gather", "debug_validate",
-    "library_path", "load_library", "VARIANTS", "MAX_SLICES", "version",
+    "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
+    "new_workspace",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libneoattn.so")
 
 VARIANTS = {"auto": 0, "valu": 1, "mfma": 2}
+SCHEDULES = {"auto": 0, "fused": 1, "staged": 2}
 MAX_SLICES = 4096
 STATUS = {0: "NEO_OK", 1: "NEO_ERR_INVALID_ARG", 2: "NEO_ERR_UNSUPPORTED",
           3: "NEO_ERR_WORKSPACE", 4: "NEO_ERR_HIP"}
@@ -78,11 +80,13 @@ def load_library():
         lib.neo_decode_attention.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S, P]
         lib.neo_decode_attention.restype = ctypes.c_int
         lib.neo_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S,
-                                                I, I, P]
+                                                I, I, I, P]
         lib.neo_decode_attention_ex.restype = ctypes.c_int
         lib.neo_decode_attention_events.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P,
-                                                    S, I, I, P, P, P]
+                                                    S, I, I, I, P, P, P]
         lib.neo_decode_attention_events.restype = ctypes.c_int
+        lib.neo_decode_workspace_init.argtypes = [P, S, P]
+        lib.neo_decode_workspace_init.restype = ctypes.c_int
         lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, P, P]
         lib.neo_paged_gather.restype = ctypes.c_int
         lib.neo_debug_validate.argtypes = [P, P, I, I, I, I, P, P]
@@ -139,26 +143,37 @@ def _stream_handle(stream, device):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def new_workspace(batch: int, num_q_heads: int, num_kv_heads: int, device="cuda",
+                  head_dim: int = 128):
+    """A zero-filled workspace (uint8 GPU tensor) sized for these shapes."""
+    torch = _torch()
+    return torch.zeros(workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim),
+                       dtype=torch.uint8, device=device)
+
+
 def _workspace(nbytes: int, device, stream_handle):
     torch = _torch()
     key = (device.index, stream_handle.value)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
         _workspaces[key] = ws
     return ws
 
 
 def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out=None, *,
-                     workspace=None, variant: str = "auto", max_slices: int = 0, stream=None):
+                     workspace=None, variant: str = "auto", schedule: str = "auto",
+                     max_slices: int = 0, stream=None):
     """Decode attention of the whole ragged batch; returns ``out`` (fp32 [B, Hq, 128]).
 
     ``scale`` defaults to 1/sqrt(head_dim). ``variant`` picks the kernel family
-    ("auto", "valu", "mfma"); ``max_slices`` caps the sequence slices of the
-    plan (0 = library default, 1 = never split a request). ``workspace`` (a
-    uint8 GPU tensor of at least ``workspace_bytes(...)``) is allocated and
-    cached per device and stream when omitted. Runs on ``stream`` (default:
-    torch's current stream) without synchronising.
+    ("auto", "valu", "mfma"); ``schedule`` the launch ("auto"/"fused": one
+    kernel, "staged": plan, decode and combine kernels); ``max_slices`` caps
+    the sequence slices of the plan (0 = library default, 1 = never split a
+    request). ``workspace`` (a zero-filled uint8 GPU tensor of at least
+    ``workspace_bytes(...)``, see ``new_workspace``) is allocated and cached per
+    device and stream when omitted. Runs on ``stream`` (default: torch's
+    current stream) without synchronising.
     """
     torch = _torch()
     lib = load_library()
@@ -189,6 +204,8 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
             raise ValueError("out must be fp32 [batch, num_q_heads, head_dim] on q's device")
     if variant not in VARIANTS:
         raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
+    if schedule not in SCHEDULES:
+        raise ValueError(f"schedule must be one of {sorted(SCHEDULES)}")
     sh = _stream_handle(stream, device)
     if B == 0:
         return out
@@ -202,7 +219,7 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
             q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
             seq_lens.data_ptr(), Hq, Hkv, D, bs, float(scale), out.data_ptr(), B,
             block_table.shape[1], NB, workspace.data_ptr(), workspace.numel(),
-            VARIANTS[variant], int(max_slices), sh))
+            VARIANTS[variant], SCHEDULES[schedule], int(max_slices), sh))
     return out
 
 

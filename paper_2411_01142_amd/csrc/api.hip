@@ -76,8 +76,9 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        float* out, int32_t batch, int32_t max_blocks_per_seq,
                                        int32_t num_blocks, void* workspace,
                                        size_t workspace_bytes, int32_t variant,
-                                       int32_t max_slices, void* decode_start_event,
-                                       void* decode_end_event, void* stream) {
+                                       int32_t schedule, int32_t max_slices,
+                                       void* decode_start_event, void* decode_end_event,
+                                       void* stream) {
   if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
   if (st != NEO_OK) return st;
@@ -87,6 +88,9 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (!isfinite(scale)) return fail(NEO_ERR_INVALID_ARG, "scale is not finite");
   if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
     return fail(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
+  if (schedule != NEO_SCHEDULE_AUTO && schedule != NEO_SCHEDULE_FUSED &&
+      schedule != NEO_SCHEDULE_STAGED)
+    return fail(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
   if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
     return fail(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
                 NEO_MAX_SLICES);
@@ -113,9 +117,10 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (!aligned(workspace, 256))
     return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
-  int32_t slices = max_slices == 0 ? kDefaultSlices : max_slices;
+  const int32_t slices = max_slices == 0 ? kDefaultSlices : max_slices;
   const int32_t min_tiles = max_slices == 0 ? kMinTilesPerSlice : 1;
   if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
+  const bool fused = schedule != NEO_SCHEDULE_STAGED;
 
   char* ws = static_cast<char*>(workspace);
   neo::DecodeParams p;
@@ -129,33 +134,41 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   p.starts = reinterpret_cast<const neo::SliceStart*>(ws + wl.starts);
   p.part_lse = reinterpret_cast<float*>(ws + wl.part_lse);
   p.part_o = reinterpret_cast<float*>(ws + wl.part_o);
+  p.counters = reinterpret_cast<int32_t*>(ws + wl.counters);
   p.batch = batch;
   p.hq = num_q_heads;
   p.hkv = num_kv_heads;
   p.mbps = max_blocks_per_seq;
   p.num_blocks = num_blocks;
+  p.max_slices = slices;
+  p.min_tiles = min_tiles;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices,
-                                  min_tiles, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
-                                  reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
-                                  reinterpret_cast<int32_t*>(ws + wl.prefix), s);
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  hipError_t e;
+  if (!fused) {
+    e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices, min_tiles,
+                         reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
+                         reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
+                         reinterpret_cast<int32_t*>(ws + wl.prefix), s);
+    if (e != hipSuccess) return fail(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  }
   const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
   if (decode_start_event) {
     e = hipEventRecord(static_cast<hipEvent_t>(decode_start_event), s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
-  e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, grid, s)
-                                  : neo::launch_decode_mfma(p, group, grid, s);
+  e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, fused, grid, s)
+                                  : neo::launch_decode_mfma(p, group, fused, grid, s);
   if (e != hipSuccess) return fail(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   if (decode_end_event) {
     e = hipEventRecord(static_cast<hipEvent_t>(decode_end_event), s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
-  e = neo::launch_combine(p, group, grid, s);
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+  if (!fused) {
+    e = neo::launch_combine(p, group, grid, s);
+    if (e != hipSuccess) return fail(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+  }
   return ok();
 }
 
@@ -165,11 +178,11 @@ neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const voi
                                    int32_t block_size, float scale, float* out, int32_t batch,
                                    int32_t max_blocks_per_seq, int32_t num_blocks,
                                    void* workspace, size_t workspace_bytes, int32_t variant,
-                                   int32_t max_slices, void* stream) {
+                                   int32_t schedule, int32_t max_slices, void* stream) {
   return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                      num_kv_heads, head_dim, block_size, scale, out, batch,
                                      max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
-                                     variant, max_slices, nullptr, nullptr, stream);
+                                     variant, schedule, max_slices, nullptr, nullptr, stream);
 }
 
 neo_status neo_decode_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -181,7 +194,18 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
   return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                      num_kv_heads, head_dim, block_size, scale, out, batch,
                                      max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
-                                     NEO_VARIANT_AUTO, 0, nullptr, nullptr, stream);
+                                     NEO_VARIANT_AUTO, NEO_SCHEDULE_AUTO, 0, nullptr, nullptr,
+                                     stream);
+}
+
+neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace) return fail(NEO_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned(workspace, 256))
+    return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  hipError_t e = neo::launch_fill_zero(workspace, workspace_bytes & ~(size_t)3,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "fill launch: %s", hipGetErrorString(e));
+  return ok();
 }
 
 neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* block_table,

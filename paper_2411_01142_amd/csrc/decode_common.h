@@ -1,7 +1,17 @@
-// Device helpers shared by the two decode-kernel families: the slice walk over
-// (request, kv head, block) tiles, the block-table cursor and the zero rows of
-// empty requests.
+// The decode driver shared by both kernel families: how a wavefront finds its
+// slice of the batch, walks (request, kv head, block) tiles with loads
+// issued ahead of use, and where a finished segment's result goes (straight
+// to `out`, or to a partial slot that the last contributor merges).
+//
+// Tiles are numbered request-major, kv-head-next, block-minor; with T tiles
+// and n slices, slice s owns [floor(sT/n), floor((s+1)T/n)). A (request, kv
+// head) pair whose tiles cross a slice boundary is "cut": every slice that
+// touches it writes a partial output normalised over its share plus the
+// log-sum-exp of its scores, and the pair is aggregated afterwards (the
+// block-granular split and per-request aggregation of Sec. 4 of the paper).
 #pragma once
+
+#include <math.h>
 
 #include "neo_internal.h"
 
@@ -15,8 +25,140 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Requests with no tokens get a zero row; every wavefront of the grid takes a
-// strided share of the batch.
+// ----------------------------------------------------------------- slice geometry
+
+__device__ inline int32_t slice_first_tile(int64_t s, int32_t T, int32_t n) {
+  return (int32_t)((s * T) / n);
+}
+// The slice holding tile t: the largest s with floor(sT/n) <= t.
+__device__ inline int32_t slice_of_tile(int32_t t, int32_t T, int32_t n) {
+  return (int32_t)((((int64_t)t + 1) * n - 1) / T);
+}
+// Partial slot of slice w for a pair starting at tile pair_first: a slice's
+// first segment uses 2w, a later (end-cut) segment 2w+1. At most one of each.
+__device__ inline int partial_slot(int32_t w, int32_t slice_first, int32_t pair_first) {
+  return slice_first >= pair_first ? 2 * w : 2 * w + 1;
+}
+
+__device__ inline int32_t slice_count(int32_t T, int32_t min_tiles, int32_t max_slices) {
+  return T > 0 ? min(max(T / min_tiles, 1), max_slices) : 0;
+}
+
+struct SliceInfo {
+  int32_t T, n;      // total tiles, slices
+  int32_t s0, s1;    // this slice's tile range
+  int32_t b, g, j;   // coordinates of tile s0
+};
+
+// ----------------------------------------------------------------- wave helpers
+
+__device__ inline int32_t wave_sum_i32(int32_t v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ inline float wave_max_f32(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ inline float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ inline int32_t wave_incl_scan_i32(int32_t v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int32_t u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// ----------------------------------------------------------------- planning
+
+// Slice from the plan kernel's output (staged launch).
+__device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
+  SliceInfo si;
+  si.T = p.hdr->total_tiles;
+  si.n = p.hdr->n_slices;
+  if (wave >= si.n) return si;
+  const SliceStart a = p.starts[wave];
+  si.s0 = a.tile;
+  si.s1 = p.starts[wave + 1].tile;
+  si.b = a.b;
+  si.g = a.g;
+  si.j = a.j;
+  return si;
+}
+
+// Slice computed by the wavefront itself from seq_lens (fused launch): a
+// wave-wide reduction of the block counts gives T; a wave-wide scan locates
+// the request holding the slice's first tile. Requests are read 64 per lane
+// group, up to kPlanRegs groups per load round.
+constexpr int kPlanRegs = 16;
+
+__device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int lane) {
+  SliceInfo si;
+  constexpr int kChunk = kWave * kPlanRegs;
+  int32_t nb[kPlanRegs];
+  int32_t total = 0;
+  for (int base = 0; base < p.batch; base += kChunk) {
+#pragma unroll
+    for (int r = 0; r < kPlanRegs; ++r) {
+      const int b = base + r * kWave + lane;
+      nb[r] = b < p.batch ? blocks_of(p.lens[b], p.mbps) : 0;
+    }
+    int32_t s = 0;
+#pragma unroll
+    for (int r = 0; r < kPlanRegs; ++r) s += nb[r];
+    total += wave_sum_i32(s);
+  }
+  si.T = total * p.hkv;
+  si.n = slice_count(si.T, p.min_tiles, p.max_slices);
+  if (wave >= si.n) return si;
+  si.s0 = slice_first_tile(wave, si.T, si.n);
+  si.s1 = slice_first_tile((int64_t)wave + 1, si.T, si.n);
+
+  // Request b holds tiles [hkv*P_b, hkv*P_{b+1}) with P the block prefix sum.
+  const int32_t u = si.s0 / p.hkv;
+  int32_t carry = 0;
+  int32_t found_b = -1, found_p = 0;
+  for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
+    if (p.batch > kChunk) {
+#pragma unroll
+      for (int r = 0; r < kPlanRegs; ++r) {
+        const int b = base + r * kWave + lane;
+        nb[r] = b < p.batch ? blocks_of(p.lens[b], p.mbps) : 0;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kPlanRegs; ++r) {
+      if (found_b >= 0) break;
+      const int32_t cs = wave_sum_i32(nb[r]);
+      if (carry + cs > u) {
+        const int32_t incl = wave_incl_scan_i32(nb[r], lane);
+        const uint64_t hit = __ballot(carry + incl > u);
+        const int first = __ffsll((unsigned long long)hit) - 1;
+        found_b = base + r * kWave + first;
+        found_p = carry + __shfl(incl - nb[r], first);
+      } else {
+        carry += cs;
+      }
+    }
+  }
+  const int32_t nbb = blocks_of(p.lens[found_b], p.mbps);
+  const int32_t rem = si.s0 - p.hkv * found_p;
+  si.b = found_b;
+  si.g = rem / nbb;
+  si.j = rem % nbb;
+  return si;
+}
+
+// ----------------------------------------------------------------- outputs
+
+// Requests with no tokens get a zero row; every wavefront takes a strided share.
 __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwaves, int lane) {
   for (int b = wave; b < p.batch; b += nwaves) {
     if (clamp_len(p.lens[b], p.mbps) != 0) continue;
@@ -26,33 +168,163 @@ __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwav
   }
 }
 
-// Physical block ids of one request row, fetched 64 at a time (one per lane)
-// and handed out with a uniform readlane; ids are clamped into the pool.
-struct TableCursor {
-  const int32_t* row;
-  int32_t base, end, vals, last_block;
-  int lane;
-  __device__ TableCursor(const int32_t* row_, int32_t j0, int32_t jend, int32_t num_blocks,
-                         int lane_)
-      : row(row_), base(j0), end(jend), last_block(num_blocks - 1), lane(lane_) {
-    vals = (base + lane < end) ? row[base + lane] : 0;
-  }
-  __device__ int32_t get(int32_t jj) {
-    if (jj - base >= kWave) {
-      base += kWave;
-      vals = (base + lane < end) ? row[base + lane] : 0;
+// Merge the partials of one cut pair into out[b][g*G .. g*G+G): M = max lse,
+// out = sum_c e^(lse_c - M) o_c / sum_c e^(lse_c - M). Contributors are the
+// slices c0..c1; lane i handles contributor c0 + i (+64k) for the weights,
+// and dims 2*lane, 2*lane+1 for the sums.
+template <int G>
+__device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, int32_t pair_first,
+                                  int32_t c0, int32_t c1, int32_t T, int32_t n, int lane) {
+  const int k = c1 - c0 + 1;
+  const int d = 2 * lane;
+  for (int h = 0; h < G; ++h) {
+    float m = -INFINITY;
+    for (int base = 0; base < k; base += kWave) {
+      const int c = c0 + base + lane;
+      if (base + lane < k) {
+        const int slot = partial_slot(c, slice_first_tile(c, T, n), pair_first);
+        m = fmaxf(m, p.part_lse[slot * G + h]);
+      }
     }
-    const int32_t id = __builtin_amdgcn_readlane(vals, jj - base);
-    return (int32_t)min((uint32_t)id, (uint32_t)last_block);
+    m = wave_max_f32(m);
+    float z = 0.f, o0 = 0.f, o1 = 0.f;
+    for (int base = 0; base < k; base += kWave) {
+      const int c = c0 + base + lane;
+      float w = 0.f;
+      if (base + lane < k) {
+        const int slot = partial_slot(c, slice_first_tile(c, T, n), pair_first);
+        w = __expf(p.part_lse[slot * G + h] - m);
+      }
+      z += w;
+      const int cnt = min(kWave, k - base);
+      for (int i = 0; i < cnt; ++i) {
+        const int cc = c0 + base + i;
+        const int slot = partial_slot(cc, slice_first_tile(cc, T, n), pair_first);
+        const float wi = __shfl(w, i);
+        const float2 o = *reinterpret_cast<const float2*>(
+            p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
+        o0 = fmaf(wi, o.x, o0);
+        o1 = fmaf(wi, o.y, o1);
+      }
+    }
+    z = wave_sum_f32(z);
+    const float inv = 1.f / z;
+    float2 r;
+    r.x = o0 * inv;
+    r.y = o1 * inv;
+    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
   }
-};
+}
 
-// Where a finished segment of pair (b, g) goes: straight to `out` when the
-// segment is the whole pair, else to a partial slot of this slice. A slice's
-// first segment uses slot 2w, a segment that starts later (and so is cut by the
-// slice's end) uses 2w+1; the combine kernel recomputes the same rule.
-__device__ inline int partial_slot(int wave, int32_t slice_first_tile, int32_t pair_first_tile) {
-  return slice_first_tile >= pair_first_tile ? 2 * wave : 2 * wave + 1;
+// Fused launch: after writing its partial for a cut pair, a slice counts itself
+// in the pair's counter; the slice that completes the count merges the pair and
+// resets the counter to zero for the next call.
+template <int G>
+__device__ inline void arrive_and_merge(const DecodeParams& p, int32_t b, int32_t g,
+                                        int32_t pair_first, int32_t pair_tiles, int32_t T,
+                                        int32_t n, int lane) {
+  const int32_t c0 = slice_of_tile(pair_first, T, n);
+  const int32_t c1 = slice_of_tile(pair_first + pair_tiles - 1, T, n);
+  __threadfence();  // publish this slice's partial before counting it
+  int32_t old = 0;
+  if (lane == 0) old = atomicAdd(p.counters + c0, 1);
+  old = __shfl(old, 0);
+  if (old != c1 - c0) return;
+  __threadfence();  // see every other contributor's partial
+  if (lane == 0) atomicExch(p.counters + c0, 0);
+  merge_pair<G>(p, b, g, pair_first, c0, c1, T, n, lane);
+}
+
+// ----------------------------------------------------------------- the driver
+
+// Family provides: Tile, State, Q; load_q, init, load_tile, step, write.
+// PF tiles are in flight ahead of the one being computed.
+template <class F, int G, int PF, bool kFused>
+__device__ inline void decode_driver(const DecodeParams& p) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = threadIdx.x >> 6;
+  const int wave = blockIdx.x * kWavesPerGroup + wv;
+  const int nwaves = gridDim.x * kWavesPerGroup;
+  zero_empty_rows(p, wave, nwaves, lane);
+  const SliceInfo si = kFused ? plan_in_wave(p, wave, lane) : read_plan(p, wave);
+  if (wave >= si.n) return;
+
+  __shared__ typename F::Shared shared[kWavesPerGroup];
+  typename F::Shared& sh = shared[wv];
+  const size_t blk_stride = (size_t)p.hkv * kTileElems;
+
+  int32_t t = si.s0;
+  int b = si.b, g = si.g, j = si.j;
+  while (t < si.s1 && b < p.batch) {
+    const int32_t L = clamp_len(p.lens[b], p.mbps);
+    const int32_t nb = (L + kBlock - 1) / kBlock;
+    if (nb == 0) {
+      ++b;
+      g = 0;
+      j = 0;
+      continue;
+    }
+    const int32_t jend = min(nb, j + (si.s1 - t));
+    const int32_t pair_first = t - j;
+
+    // Block ids of this row, 64 at a time, one per lane.
+    const int32_t* trow = p.table + (size_t)b * p.mbps;
+    int32_t tbase = j;
+    int32_t tvals = (tbase + lane < jend) ? trow[tbase + lane] : 0;
+    auto tile_off = [&](int32_t jj) -> size_t {
+      if (jj - tbase >= kWave) {
+        tbase += kWave;
+        tvals = (tbase + lane < jend) ? trow[tbase + lane] : 0;
+      }
+      const int32_t id = __builtin_amdgcn_readlane(tvals, jj - tbase);
+      return (size_t)min((uint32_t)id, (uint32_t)(p.num_blocks - 1)) * blk_stride +
+             (size_t)g * kTileElems;
+    };
+
+    typename F::Q qr;
+    F::load_q(qr, p.q + ((size_t)b * p.hq + g * G) * kHeadDim, lane);
+    typename F::State st;
+    F::init(st);
+
+    typename F::Tile buf[PF + 1];
+#pragma unroll
+    for (int i = 0; i < PF; ++i)
+      if (j + i < jend) {
+        const size_t off = tile_off(j + i);
+        F::load_tile(buf[i], p.k + off, p.v + off, lane);
+      }
+    for (int32_t jj = j; jj < jend; jj += PF + 1) {
+#pragma unroll
+      for (int u = 0; u <= PF; ++u) {
+        const int32_t cur = jj + u;
+        if (cur >= jend) break;
+        const int32_t ld = cur + PF;
+        if (ld < jend) {
+          const size_t off = tile_off(ld);
+          F::load_tile(buf[(u + PF) % (PF + 1)], p.k + off, p.v + off, lane);
+        }
+        F::step(st, buf[u], qr, L - cur * kBlock, p.scale_log2, lane, sh);
+      }
+    }
+
+    if (j == 0 && jend == nb) {
+      F::write(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);
+    } else {
+      const int slot = partial_slot(wave, si.s0, pair_first);
+      F::write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G, lane);
+      if (kFused) arrive_and_merge<G>(p, b, g, pair_first, nb, si.T, si.n, lane);
+    }
+
+    t += jend - j;
+    j = jend;
+    if (j == nb) {
+      j = 0;
+      if (++g == p.hkv) {
+        g = 0;
+        ++b;
+      }
+    }
+  }
 }
 
 }  // namespace neo

@@ -36,7 +36,7 @@ struct alignas(16) SliceStart {
 };
 
 struct WorkspaceLayout {
-  size_t hdr, starts, prefix, part_lse, part_o, total;
+  size_t hdr, starts, counters, prefix, part_lse, part_o, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -51,6 +51,8 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t group) {
   off = align256(off + sizeof(PlanHeader));
   w.starts = off;
   off = align256(off + sizeof(SliceStart) * (NEO_MAX_SLICES + 1));
+  w.counters = off;  // arrival counts of cut pairs (fused launch); zero between calls
+  off = align256(off + sizeof(int32_t) * NEO_MAX_SLICES);
   w.prefix = off;
   off = align256(off + sizeof(int32_t) * ((size_t)batch + 1));
   w.part_lse = off;
@@ -81,7 +83,9 @@ struct DecodeParams {
   const SliceStart* starts;
   float* part_lse;            // [2*NEO_MAX_SLICES][group]
   float* part_o;              // [2*NEO_MAX_SLICES][group][128]
+  int32_t* counters;          // [NEO_MAX_SLICES]
   int32_t batch, hq, hkv, mbps, num_blocks;
+  int32_t max_slices, min_tiles;
   float scale_log2;           // scale * log2(e)
 };
 
@@ -89,10 +93,11 @@ struct DecodeParams {
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
                        int32_t max_slices, int32_t min_tiles, PlanHeader* hdr,
                        SliceStart* starts, int32_t* prefix, hipStream_t stream);
-hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, int32_t grid,
+hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
                               hipStream_t stream);
-hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, int32_t grid,
+hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
                               hipStream_t stream);
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hipStream_t stream);
 hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,
                          const int32_t* lens, const int32_t* offsets, int32_t batch,

@@ -7,20 +7,25 @@
 // are aggregated afterwards. Here a worker is one wavefront: the batch's tiles
 // ((request, kv head, block) triples) are laid end to end and cut into equal
 // contiguous slices, so the load is balanced whatever the length mix.
-#include <math.h>
+#include <algorithm>
 
-#include "neo_internal.h"
+#include "decode_common.h"
 
 namespace neo {
 namespace {
 
-// One workgroup: block counts, an exclusive scan over requests (tile offsets),
-// then each slice's first tile located by binary search.
+// One workgroup: block counts, an exclusive scan over requests (tile
+// offsets), then each slice's first tile located by binary search (over an
+// LDS copy of the offsets when the batch fits).
+constexpr int kPlanLdsBatch = 8192;
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t* __restrict__ lens, int32_t batch, int32_t hkv, int32_t mbps,
     int32_t max_slices, int32_t min_tiles, PlanHeader* __restrict__ hdr,
     SliceStart* __restrict__ starts, int32_t* __restrict__ prefix) {
   __shared__ int32_t sums[kPlanThreads];
+  __shared__ int32_t sprefix[kPlanLdsBatch + 1];
+  const bool in_lds = batch <= kPlanLdsBatch;
   const int tid = threadIdx.x;
   const int per = (batch + kPlanThreads - 1) / kPlanThreads;
   const int b0 = min(batch, tid * per);
@@ -37,15 +42,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
   int32_t run = tid == 0 ? 0 : sums[tid - 1];
   for (int b = b0; b < b1; ++b) {
-    prefix[b] = run * hkv;
+    if (in_lds) sprefix[b] = run * hkv;
+    else prefix[b] = run * hkv;
     run += blocks_of(lens[b], mbps);
   }
   const int32_t total = sums[kPlanThreads - 1] * hkv;
-  if (tid == 0) prefix[batch] = total;
   __syncthreads();
+  const int32_t* pre = in_lds ? sprefix : prefix;
 
-  int32_t n = 0;
-  if (total > 0) n = min(max(total / min_tiles, 1), max_slices);
+  const int32_t n = slice_count(total, min_tiles, max_slices);
   for (int s = tid; s <= n; s += kPlanThreads) {
     SliceStart st;
     if (s == n) {
@@ -54,14 +59,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       st.g = 0;
       st.j = 0;
     } else {
-      const int32_t tile = (int32_t)(((int64_t)s * total) / n);
-      int lo = 0, hi = batch - 1;  // largest b with prefix[b] <= tile
+      const int32_t tile = slice_first_tile(s, total, n);
+      int lo = 0, hi = batch - 1;  // largest b with pre[b] <= tile
       while (lo < hi) {
         int mid = (lo + hi + 1) >> 1;
-        if (prefix[mid] <= tile) lo = mid; else hi = mid - 1;
+        if (pre[mid] <= tile) lo = mid; else hi = mid - 1;
       }
       const int32_t nb = blocks_of(lens[lo], mbps);
-      const int32_t r = tile - prefix[lo];
+      const int32_t r = tile - pre[lo];
       st.tile = tile;
       st.b = lo;
       st.g = r / nb;
@@ -79,49 +84,32 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
 }
 
-// Aggregation of the partial outputs of requests cut by slice boundaries
-// (Sec. 4: "aggregate the partial outputs of each request"). Slice w owns the
-// merge of the (request, kv head) pair that starts inside it and continues
-// into slice w+1. Each contributing slice stored its part normalised, with its
-// log-sum-exp: out = sum_i e^(lse_i - M) o_i / sum_i e^(lse_i - M).
+// Staged launch: aggregation of the partial outputs of requests cut by slice
+// boundaries (Sec. 4: "aggregate the partial outputs of each request"). Slice
+// w merges the (request, kv head) pair that starts inside it and continues
+// into slice w+1; every contributing slice stored its part normalised, with
+// its log-sum-exp.
 template <int G>
 __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int w = blockIdx.x * kWavesPerGroup + (threadIdx.x >> 6);
-  const int n = p.hdr->n_slices;
+  const int32_t T = p.hdr->total_tiles;
+  const int32_t n = p.hdr->n_slices;
   if (w + 1 >= n) return;
   const SliceStart s0 = p.starts[w];
   const SliceStart s1 = p.starts[w + 1];
   if (s1.j == 0) return;                       // slice w ends on a pair boundary
-  const int32_t pair_start = s1.tile - s1.j;
-  if (pair_start < s0.tile) return;            // an earlier slice owns this pair
+  const int32_t pair_first = s1.tile - s1.j;
+  if (pair_first < s0.tile) return;            // an earlier slice owns this pair
   const int32_t nb = blocks_of(p.lens[s1.b], p.mbps);
-  const int32_t pair_end = pair_start + nb;
-  int last = w + 1;
-  while (last + 1 < n && p.starts[last + 1].tile < pair_end) ++last;
-  const int d = 2 * lane;
-  for (int h = 0; h < G; ++h) {
-    float m = -INFINITY;
-    for (int c = w; c <= last; ++c) {
-      const int slot = (p.starts[c].tile >= pair_start) ? 2 * c : 2 * c + 1;
-      m = fmaxf(m, p.part_lse[slot * G + h]);
-    }
-    float z = 0.f, o0 = 0.f, o1 = 0.f;
-    for (int c = w; c <= last; ++c) {
-      const int slot = (p.starts[c].tile >= pair_start) ? 2 * c : 2 * c + 1;
-      const float e = __expf(p.part_lse[slot * G + h] - m);
-      const float2 o = *reinterpret_cast<const float2*>(
-          p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
-      z += e;
-      o0 = fmaf(e, o.x, o0);
-      o1 = fmaf(e, o.y, o1);
-    }
-    const float inv = 1.f / z;
-    float2 r;
-    r.x = o0 * inv;
-    r.y = o1 * inv;
-    *reinterpret_cast<float2*>(p.out + ((size_t)s1.b * p.hq + s1.g * G + h) * kHeadDim + d) = r;
-  }
+  const int32_t c1 = slice_of_tile(pair_first + nb - 1, T, n);
+  merge_pair<G>(p, s1.b, s1.g, pair_first, w, c1, T, n, lane);
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* __restrict__ dst, size_t words) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < words;
+       i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = 0u;
 }
 
 // Workgroup (j, b) copies block j of request b: thread -> (slot, 8-dim piece).
@@ -198,6 +186,14 @@ hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hi
     case 16: combine_kernel<16><<<grid, block, 0, stream>>>(p); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
+  const size_t words = bytes / 4;
+  if (words == 0) return hipSuccess;
+  const size_t blocks = std::min<size_t>((words + 255) / 256, 4096);
+  fill_zero_kernel<<<(unsigned)blocks, 256, 0, stream>>>(static_cast<uint32_t*>(ptr), words);
   return hipGetLastError();
 }
 

@@ -33,6 +33,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("neo_decode_attention", "neo_decode_attention_ex", "neo_decode_workspace_bytes",
+              "neo_decode_workspace_init", "neo_decode_attention_events",
               "neo_paged_gather", "neo_debug_validate", "neo_last_error", "neo_version"):
         assert n in names
 
@@ -75,12 +76,12 @@ FAKE = 1 << 20  # non-null, 256-aligned host address; never dereferenced on thes
 def call(lib, **kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, table=FAKE, lens=FAKE, hq=32, hkv=8, d=128, bs=16,
              scale=1 / math.sqrt(128), out=FAKE, batch=4, mbps=8, nb=100, ws=FAKE,
-             ws_bytes=1 << 40, variant=0, slices=0, stream=None)
+             ws_bytes=1 << 40, variant=0, schedule=0, slices=0, stream=None)
     a.update(kw)
     return lib.neo_decode_attention_ex(a["q"], a["k"], a["v"], a["table"], a["lens"], a["hq"],
                                        a["hkv"], a["d"], a["bs"], a["scale"], a["out"],
                                        a["batch"], a["mbps"], a["nb"], a["ws"], a["ws_bytes"],
-                                       a["variant"], a["slices"], a["stream"])
+                                       a["variant"], a["schedule"], a["slices"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,code,needle", [
@@ -106,6 +107,7 @@ def call(lib, **kw):
     (dict(out=FAKE + 4), INVALID, "aligned"),
     (dict(ws=FAKE + 64), INVALID, "aligned"),
     (dict(variant=7), UNSUPPORTED, "variant"),
+    (dict(schedule=3), UNSUPPORTED, "schedule"),
     (dict(slices=-1), INVALID, "max_slices"),
     (dict(slices=100000), INVALID, "max_slices"),
     (dict(batch=1 << 20, mbps=1 << 12), INVALID, "2^31"),
@@ -138,6 +140,8 @@ def test_gather_and_validate_reject(lib):
                                 None) == OK
     assert lib.neo_debug_validate(FAKE, FAKE, 4, 0, 16, 100, FAKE, None) == INVALID
     assert lib.neo_debug_validate(None, FAKE, 4, 8, 16, 100, FAKE, None) == INVALID
+    assert lib.neo_decode_workspace_init(None, 1024, None) == INVALID
+    assert lib.neo_decode_workspace_init(FAKE + 4, 1024, None) == INVALID
 
 
 def test_python_binding_refuses_cpu_tensors():
