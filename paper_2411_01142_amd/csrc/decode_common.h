@@ -25,6 +25,26 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.6931471805599453f;
 
+// ----------------------------------------------------------------- coherent access
+
+// Partials written by one slice and merged by another (possibly on another
+// XCD, with its own L2) go through device-coherent accesses: stores that write
+// through to the coherence point and loads that read from it. Ordering against
+// the arrival counter comes from waiting for every store to complete before
+// the counter is incremented, instead of a device-scope fence (which writes
+// back and invalidates the whole L2).
+__device__ inline void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void wait_all_memory() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // ----------------------------------------------------------------- slice geometry
 
 __device__ inline int32_t slice_first_tile(int64_t s, int32_t T, int32_t n) {
@@ -99,17 +119,25 @@ __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
 // group, up to kPlanRegs groups per load round.
 constexpr int kPlanRegs = 16;
 
+// Block counts of requests base + 64r + lane, r < kPlanRegs (0 past the batch).
+// Loads use a clamped index so that all of them issue before any is waited on.
+__device__ inline void load_block_counts(const DecodeParams& p, int base, int lane,
+                                         int32_t (&nb)[kPlanRegs]) {
+  int32_t raw[kPlanRegs];
+#pragma unroll
+  for (int r = 0; r < kPlanRegs; ++r) raw[r] = p.lens[min(base + r * kWave + lane, p.batch - 1)];
+#pragma unroll
+  for (int r = 0; r < kPlanRegs; ++r)
+    nb[r] = (base + r * kWave + lane < p.batch) ? blocks_of(raw[r], p.mbps) : 0;
+}
+
 __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int lane) {
   SliceInfo si;
   constexpr int kChunk = kWave * kPlanRegs;
   int32_t nb[kPlanRegs];
   int32_t total = 0;
   for (int base = 0; base < p.batch; base += kChunk) {
-#pragma unroll
-    for (int r = 0; r < kPlanRegs; ++r) {
-      const int b = base + r * kWave + lane;
-      nb[r] = b < p.batch ? blocks_of(p.lens[b], p.mbps) : 0;
-    }
+    load_block_counts(p, base, lane, nb);
     int32_t s = 0;
 #pragma unroll
     for (int r = 0; r < kPlanRegs; ++r) s += nb[r];
@@ -126,13 +154,7 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   int32_t carry = 0;
   int32_t found_b = -1, found_p = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
-    if (p.batch > kChunk) {
-#pragma unroll
-      for (int r = 0; r < kPlanRegs; ++r) {
-        const int b = base + r * kWave + lane;
-        nb[r] = b < p.batch ? blocks_of(p.lens[b], p.mbps) : 0;
-      }
-    }
+    if (p.batch > kChunk) load_block_counts(p, base, lane, nb);
 #pragma unroll
     for (int r = 0; r < kPlanRegs; ++r) {
       if (found_b >= 0) break;
@@ -170,49 +192,87 @@ __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwav
 
 // Merge the partials of one cut pair into out[b][g*G .. g*G+G): M = max lse,
 // out = sum_c e^(lse_c - M) o_c / sum_c e^(lse_c - M). Contributors are the
-// slices c0..c1; lane i handles contributor c0 + i (+64k) for the weights,
-// and dims 2*lane, 2*lane+1 for the sums.
+// slices c0..c1. Each lane owns dims 2*lane, 2*lane+1 of the sums.
+template <int G>
+__device__ inline int contributor_slot(int32_t c, int32_t T, int32_t n, int32_t pair_first) {
+  return partial_slot(c, slice_first_tile(c, T, n), pair_first);
+}
+
+template <int G>
+__device__ inline void store_merged(const DecodeParams& p, int32_t b, int32_t g, int h, int d,
+                                    float a0, float a1, float z) {
+  const float inv = 1.f / z;
+  float2 r;
+  r.x = a0 * inv;
+  r.y = a1 * inv;
+  *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
+}
+
 template <int G>
 __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, int32_t pair_first,
                                   int32_t c0, int32_t c1, int32_t T, int32_t n, int lane) {
   const int k = c1 - c0 + 1;
   const int d = 2 * lane;
+  if (k <= kWave) {
+    // Lane i reads the log-sum-exps of contributor c0 + i; partial rows are
+    // then read kBatch contributors at a time with all loads issued together.
+    constexpr int kBatch = 16 / G > 0 ? 16 / G : 1;  // 32 registers of partial rows
+    const int mine = lane < k ? lane : 0;
+    const int my_slot = contributor_slot<G>(c0 + mine, T, n, pair_first);
+    float w[G], a0[G], a1[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float lse = lane < k ? load_coherent(p.part_lse + my_slot * G + h) : -INFINITY;
+      w[h] = __expf(lse - wave_max_f32(lse));
+      a0[h] = a1[h] = 0.f;
+    }
+    for (int i0 = 0; i0 < k; i0 += kBatch) {
+      float ov[kBatch][G][2];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int slot = contributor_slot<G>(c0 + min(i0 + u, k - 1), T, n, pair_first);
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
+          ov[u][h][0] = load_coherent(o);
+          ov[u][h][1] = load_coherent(o + 1);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (i0 + u >= k) break;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float wi = __shfl(w[h], i0 + u);
+          a0[h] = fmaf(wi, ov[u][h][0], a0[h]);
+          a1[h] = fmaf(wi, ov[u][h][1], a1[h]);
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) store_merged<G>(p, b, g, h, d, a0[h], a1[h], wave_sum_f32(w[h]));
+    return;
+  }
+  // More than 64 contributors (a very long request cut into many slices):
+  // global maximum first, then the weighted sums, one contributor at a time.
   for (int h = 0; h < G; ++h) {
     float m = -INFINITY;
-    for (int base = 0; base < k; base += kWave) {
-      const int c = c0 + base + lane;
-      if (base + lane < k) {
-        const int slot = partial_slot(c, slice_first_tile(c, T, n), pair_first);
-        m = fmaxf(m, p.part_lse[slot * G + h]);
-      }
-    }
+    for (int base = 0; base < k; base += kWave)
+      if (base + lane < k)
+        m = fmaxf(m, load_coherent(p.part_lse +
+                                   contributor_slot<G>(c0 + base + lane, T, n, pair_first) * G +
+                                   h));
     m = wave_max_f32(m);
-    float z = 0.f, o0 = 0.f, o1 = 0.f;
-    for (int base = 0; base < k; base += kWave) {
-      const int c = c0 + base + lane;
-      float w = 0.f;
-      if (base + lane < k) {
-        const int slot = partial_slot(c, slice_first_tile(c, T, n), pair_first);
-        w = __expf(p.part_lse[slot * G + h] - m);
-      }
-      z += w;
-      const int cnt = min(kWave, k - base);
-      for (int i = 0; i < cnt; ++i) {
-        const int cc = c0 + base + i;
-        const int slot = partial_slot(cc, slice_first_tile(cc, T, n), pair_first);
-        const float wi = __shfl(w, i);
-        const float2 o = *reinterpret_cast<const float2*>(
-            p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
-        o0 = fmaf(wi, o.x, o0);
-        o1 = fmaf(wi, o.y, o1);
-      }
+    float z = 0.f, a0 = 0.f, a1 = 0.f;
+    for (int i = 0; i < k; ++i) {
+      const int slot = contributor_slot<G>(c0 + i, T, n, pair_first);
+      const float wi = __expf(load_coherent(p.part_lse + slot * G + h) - m);
+      const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
+      z += wi;
+      a0 = fmaf(wi, load_coherent(o), a0);
+      a1 = fmaf(wi, load_coherent(o + 1), a1);
     }
-    z = wave_sum_f32(z);
-    const float inv = 1.f / z;
-    float2 r;
-    r.x = o0 * inv;
-    r.y = o1 * inv;
-    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
+    store_merged<G>(p, b, g, h, d, a0, a1, z);
   }
 }
 
@@ -225,13 +285,14 @@ __device__ inline void arrive_and_merge(const DecodeParams& p, int32_t b, int32_
                                         int32_t n, int lane) {
   const int32_t c0 = slice_of_tile(pair_first, T, n);
   const int32_t c1 = slice_of_tile(pair_first + pair_tiles - 1, T, n);
-  __threadfence();  // publish this slice's partial before counting it
+  wait_all_memory();  // this slice's partial has reached the coherence point
   int32_t old = 0;
-  if (lane == 0) old = atomicAdd(p.counters + c0, 1);
+  if (lane == 0)
+    old = __hip_atomic_fetch_add(p.counters + c0, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0);
   if (old != c1 - c0) return;
-  __threadfence();  // see every other contributor's partial
-  if (lane == 0) atomicExch(p.counters + c0, 0);
+  if (lane == 0)
+    __hip_atomic_store(p.counters + c0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   merge_pair<G>(p, b, g, pair_first, c0, c1, T, n, lane);
 }
 
@@ -308,10 +369,11 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     }
 
     if (j == 0 && jend == nb) {
-      F::write(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);
+      F::template write<false>(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);
     } else {
       const int slot = partial_slot(wave, si.s0, pair_first);
-      F::write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G, lane);
+      F::template write<true>(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
+                              lane);
       if (kFused) arrive_and_merge<G>(p, b, g, pair_first, nb, si.T, si.n, lane);
     }
 

@@ -64,12 +64,16 @@ struct MfmaFamily {
   __device__ static void load_tile(Tile& x, const uint16_t* __restrict__ kbase,
                                    const uint16_t* __restrict__ vbase, int lane) {
     const int col = lane & 15, rq = lane >> 4;
+    // Each KV tile is read exactly once: nontemporal loads keep it from
+    // displacing reusable lines in the caches.
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
-      x.k[kb] = *reinterpret_cast<const bf16x8_t*>(kbase + kPiece * (kWave * kb + lane));
+      x.k[kb] = __builtin_nontemporal_load(
+          reinterpret_cast<const bf16x8_t*>(kbase + kPiece * (kWave * kb + lane)));
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb)
-      x.v[mb] = *reinterpret_cast<const s16x4_t*>(vbase + (16 * mb + col) * kBlock + 4 * rq);
+      x.v[mb] = __builtin_nontemporal_load(
+          reinterpret_cast<const s16x4_t*>(vbase + (16 * mb + col) * kBlock + 4 * rq));
   }
 
   __device__ static void step(State& st, Tile& x, const Q& q, int32_t valid, float scale_log2,
@@ -119,7 +123,9 @@ struct MfmaFamily {
     }
   }
 
-  // rows: [G][128] destination (normalised); lse: [G] natural-log log-sum-exp or null.
+  // rows: [G][128] destination (normalised); lse: [G] natural-log log-sum-exp or
+  // null. kCoherent: partials another slice will merge (device-coherent stores).
+  template <bool kCoherent>
   __device__ static void write(const State& st, float* __restrict__ rows,
                                float* __restrict__ lse, int lane) {
     const int col = lane & 15, rq = lane >> 4;
@@ -129,8 +135,19 @@ struct MfmaFamily {
     if (col < G) {
       float* r = rows + col * kHeadDim + 4 * rq;
 #pragma unroll
-      for (int mb = 0; mb < 8; ++mb) *reinterpret_cast<f32x4_t*>(r + 16 * mb) = st.acc[mb] * inv;
-      if (lse && rq == 0) lse[col] = (st.m + __log2f(lt)) * kLn2;
+      for (int mb = 0; mb < 8; ++mb) {
+        const f32x4_t v = st.acc[mb] * inv;
+        if (kCoherent) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) store_coherent(r + 16 * mb + i, v[i]);
+        } else {
+          *reinterpret_cast<f32x4_t*>(r + 16 * mb) = v;
+        }
+      }
+      if (lse && rq == 0) {
+        const float x = (st.m + __log2f(lt)) * kLn2;
+        if (kCoherent) store_coherent(lse + col, x); else lse[col] = x;
+      }
     }
   }
 };

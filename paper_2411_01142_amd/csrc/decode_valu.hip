@@ -89,10 +89,12 @@ struct ValuFamily {
     const int r = lane >> 4, c = lane & 15;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      x.k[i] = *reinterpret_cast<const u32x4_t*>(kbase + (c * kBlock + 4 * i + r) * kPiece);
+      x.k[i] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(kbase + (c * kBlock + 4 * i + r) * kPiece));
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      x.v[i] = *reinterpret_cast<const u32x4_t*>(vbase + 512 * i + 8 * lane);
+      x.v[i] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(vbase + 512 * i + 8 * lane));
   }
 
   __device__ static void step(State& st, Tile& x, const Q& q, int32_t valid, float scale_log2,
@@ -163,6 +165,7 @@ struct ValuFamily {
     wave_sync_lds();
   }
 
+  template <bool kCoherent>
   __device__ static void write(const State& st, float* __restrict__ rows,
                                float* __restrict__ lse, int lane) {
 #pragma unroll
@@ -174,9 +177,15 @@ struct ValuFamily {
       for (int i = 0; i < 4; ++i) {
         const float a =
             st.acc[i][h] + __builtin_amdgcn_update_dpp(0.f, st.acc[i][h], 0xB1, 0xF, 0xF, false);
-        if ((lane & 1) == 0) rows[h * kHeadDim + 32 * i + (lane >> 1)] = a * inv;
+        if ((lane & 1) == 0) {
+          float* dst = rows + h * kHeadDim + 32 * i + (lane >> 1);
+          if (kCoherent) store_coherent(dst, a * inv); else *dst = a * inv;
+        }
       }
-      if (lse && lane == 0) lse[h] = (st.m[h] + __log2f(lt)) * kLn2;
+      if (lse && lane == 0) {
+        const float x = (st.m[h] + __log2f(lt)) * kLn2;
+        if (kCoherent) store_coherent(lse + h, x); else lse[h] = x;
+      }
     }
   }
 };
