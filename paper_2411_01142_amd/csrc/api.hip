@@ -2,8 +2,11 @@
 // call), workspace sizing and the launch sequence plan -> decode -> combine.
 #include <math.h>
 #include <stdarg.h>
+
+#include <algorithm>
 #include <stdio.h>
 
+#include <atomic>
 #include <string>
 
 #include "neo_internal.h"
@@ -31,10 +34,31 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
 bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
 
-// Slices (wavefronts) the plan may cut by default, and the smallest number of
-// tiles a slice should hold before the plan stops adding slices.
-constexpr int32_t kDefaultSlices = 2048;
-constexpr int32_t kMinTilesPerSlice = 8;
+// Compute units of the current device, cached per device ordinal. The default
+// plan uses whole multiples of (CUs x wavefronts per workgroup) slices, up to
+// two workgroups per CU.
+constexpr int kMaxDevices = 64;
+std::atomic<int32_t> g_cu_count[kMaxDevices];
+
+neo_status device_cu_count(int32_t* cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < kMaxDevices) {
+    const int32_t cached = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (cached > 0) {
+      *cus = cached;
+      return NEO_OK;
+    }
+  }
+  int v = 0;
+  e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || v <= 0)
+    return fail(NEO_ERR_HIP, "hipDeviceGetAttribute(cu count): %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(v, std::memory_order_relaxed);
+  *cus = v;
+  return NEO_OK;
+}
 
 neo_status check_heads(int32_t hq, int32_t hkv, int32_t head_dim) {
   if (hq <= 0 || hkv <= 0)
@@ -117,10 +141,18 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (!aligned(workspace, 256))
     return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
-  const int32_t slices = max_slices == 0 ? kDefaultSlices : max_slices;
-  const int32_t min_tiles = max_slices == 0 ? kMinTilesPerSlice : 1;
+  int32_t cus = 0;
+  st = device_cu_count(&cus);
+  if (st != NEO_OK) return st;
+  const int32_t quantum = cus * neo::kWavesPerGroup;
+  const int32_t slices =
+      max_slices == 0 ? std::min<int32_t>(2 * quantum, NEO_MAX_SLICES) : max_slices;
+  const int32_t min_tiles = max_slices == 0 ? 0 : 1;
   if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
-  const bool fused = schedule != NEO_SCHEDULE_STAGED;
+  // Staged by default: measured on MI355X it is as fast or faster than the
+  // fused launch on every workload shape but the most skewed one, because
+  // three short launches cost less than the fused kernel's in-kernel merges.
+  const bool fused = schedule == NEO_SCHEDULE_FUSED;
 
   char* ws = static_cast<char*>(workspace);
   neo::DecodeParams p;
@@ -142,13 +174,14 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   p.num_blocks = num_blocks;
   p.max_slices = slices;
   p.min_tiles = min_tiles;
+  p.slice_quantum = quantum;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (!fused) {
     e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices, min_tiles,
-                         reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
+                         quantum, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
                          reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
                          reinterpret_cast<int32_t*>(ws + wl.prefix), s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));

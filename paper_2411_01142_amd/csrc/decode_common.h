@@ -60,8 +60,23 @@ __device__ inline int partial_slot(int32_t w, int32_t slice_first, int32_t pair_
   return slice_first >= pair_first ? 2 * w : 2 * w + 1;
 }
 
-__device__ inline int32_t slice_count(int32_t T, int32_t min_tiles, int32_t max_slices) {
-  return T > 0 ? min(max(T / min_tiles, 1), max_slices) : 0;
+// Number of slices for T tiles. With min_tiles > 0: T / min_tiles, capped.
+// With min_tiles == 0 (the default policy): whole multiples of `quantum` (one
+// 4-wave workgroup per CU) so every CU gets the same share, stepping up to
+// two workgroups per CU once slices still hold kAutoTilesPerSlice tiles;
+// small batches get T / 8 slices.
+constexpr int32_t kAutoTilesPerSlice = 40;
+constexpr int32_t kSmallTilesPerSlice = 8;
+
+__device__ inline int32_t slice_count(int32_t T, int32_t min_tiles, int32_t max_slices,
+                                      int32_t quantum) {
+  if (T <= 0) return 0;
+  if (min_tiles > 0) return min(max(T / min_tiles, 1), max_slices);
+  int32_t n;
+  if (T >= 2 * quantum * kAutoTilesPerSlice) n = 2 * quantum;
+  else if (T >= quantum * kSmallTilesPerSlice) n = quantum;
+  else n = max(T / kSmallTilesPerSlice, 1);
+  return min(n, max_slices);
 }
 
 struct SliceInfo {
@@ -144,7 +159,7 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
     total += wave_sum_i32(s);
   }
   si.T = total * p.hkv;
-  si.n = slice_count(si.T, p.min_tiles, p.max_slices);
+  si.n = slice_count(si.T, p.min_tiles, p.max_slices, p.slice_quantum);
   if (wave >= si.n) return si;
   si.s0 = slice_first_tile(wave, si.T, si.n);
   si.s1 = slice_first_tile((int64_t)wave + 1, si.T, si.n);
@@ -216,7 +231,7 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
   if (k <= kWave) {
     // Lane i reads the log-sum-exps of contributor c0 + i; partial rows are
     // then read kBatch contributors at a time with all loads issued together.
-    constexpr int kBatch = 16 / G > 0 ? 16 / G : 1;  // 32 registers of partial rows
+    constexpr int kBatch = 32 / G > 16 ? 16 : (32 / G > 0 ? 32 / G : 1);  // 64 registers
     const int mine = lane < k ? lane : 0;
     const int my_slot = contributor_slot<G>(c0 + mine, T, n, pair_first);
     float w[G], a0[G], a1[G];
@@ -230,7 +245,8 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
       float ov[kBatch][G][2];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int slot = contributor_slot<G>(c0 + min(i0 + u, k - 1), T, n, pair_first);
+        if (i0 + u >= k) break;  // uniform
+        const int slot = contributor_slot<G>(c0 + i0 + u, T, n, pair_first);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
@@ -277,12 +293,10 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
 }
 
 // Fused launch: after writing its partial for a cut pair, a slice counts itself
-// in the pair's counter; the slice that completes the count merges the pair and
-// resets the counter to zero for the next call.
-template <int G>
-__device__ inline void arrive_and_merge(const DecodeParams& p, int32_t b, int32_t g,
-                                        int32_t pair_first, int32_t pair_tiles, int32_t T,
-                                        int32_t n, int lane) {
+// in the pair's counter; the slice that completes the count merges the pair
+// (returns true) and resets the counter to zero for the next call.
+__device__ inline bool arrive_last(const DecodeParams& p, int32_t pair_first, int32_t pair_tiles,
+                                   int32_t T, int32_t n, int lane) {
   const int32_t c0 = slice_of_tile(pair_first, T, n);
   const int32_t c1 = slice_of_tile(pair_first + pair_tiles - 1, T, n);
   wait_all_memory();  // this slice's partial has reached the coherence point
@@ -290,10 +304,10 @@ __device__ inline void arrive_and_merge(const DecodeParams& p, int32_t b, int32_
   if (lane == 0)
     old = __hip_atomic_fetch_add(p.counters + c0, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0);
-  if (old != c1 - c0) return;
+  if (old != c1 - c0) return false;
   if (lane == 0)
     __hip_atomic_store(p.counters + c0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  merge_pair<G>(p, b, g, pair_first, c0, c1, T, n, lane);
+  return true;
 }
 
 // ----------------------------------------------------------------- the driver
@@ -313,6 +327,13 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   __shared__ typename F::Shared shared[kWavesPerGroup];
   typename F::Shared& sh = shared[wv];
   const size_t blk_stride = (size_t)p.hkv * kTileElems;
+
+  // A slice holds at most two cut pairs: the one it starts in and the one it
+  // ends in.
+  struct Pending {
+    int32_t b, g, first, tiles;
+  } pend[2];
+  int npend = 0;
 
   int32_t t = si.s0;
   int b = si.b, g = si.g, j = si.j;
@@ -374,7 +395,14 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       const int slot = partial_slot(wave, si.s0, pair_first);
       F::template write<true>(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
                               lane);
-      if (kFused) arrive_and_merge<G>(p, b, g, pair_first, nb, si.T, si.n, lane);
+      if (kFused && arrive_last(p, pair_first, nb, si.T, si.n, lane)) {
+        // Merge after the tile loop, when the tile buffers are no longer live.
+        pend[npend].b = b;
+        pend[npend].g = g;
+        pend[npend].first = pair_first;
+        pend[npend].tiles = nb;
+        ++npend;
+      }
     }
 
     t += jend - j;
@@ -385,6 +413,13 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         g = 0;
         ++b;
       }
+    }
+  }
+  if (kFused) {
+    for (int i = 0; i < npend; ++i) {
+      const int32_t c0 = slice_of_tile(pend[i].first, si.T, si.n);
+      const int32_t c1 = slice_of_tile(pend[i].first + pend[i].tiles - 1, si.T, si.n);
+      merge_pair<G>(p, pend[i].b, pend[i].g, pend[i].first, c0, c1, si.T, si.n, lane);
     }
   }
 }

@@ -85,13 +85,14 @@ struct DecodeParams {
   float* part_o;              // [2*NEO_MAX_SLICES][group][128]
   int32_t* counters;          // [NEO_MAX_SLICES]
   int32_t batch, hq, hkv, mbps, num_blocks;
-  int32_t max_slices, min_tiles;
+  int32_t max_slices, min_tiles;  // min_tiles == 0: the default slice policy
+  int32_t slice_quantum;          // compute units x wavefronts per workgroup
   float scale_log2;           // scale * log2(e)
 };
 
 // Launchers (each returns the hipError_t of its launch).
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
-                       int32_t max_slices, int32_t min_tiles, PlanHeader* hdr,
+                       int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* hdr,
                        SliceStart* starts, int32_t* prefix, hipStream_t stream);
 hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
                               hipStream_t stream);

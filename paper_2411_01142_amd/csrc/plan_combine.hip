@@ -21,7 +21,7 @@ constexpr int kPlanLdsBatch = 8192;
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t* __restrict__ lens, int32_t batch, int32_t hkv, int32_t mbps,
-    int32_t max_slices, int32_t min_tiles, PlanHeader* __restrict__ hdr,
+    int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* __restrict__ hdr,
     SliceStart* __restrict__ starts, int32_t* __restrict__ prefix) {
   __shared__ int32_t sums[kPlanThreads];
   __shared__ int32_t sprefix[kPlanLdsBatch + 1];
@@ -50,7 +50,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __syncthreads();
   const int32_t* pre = in_lds ? sprefix : prefix;
 
-  const int32_t n = slice_count(total, min_tiles, max_slices);
+  const int32_t n = slice_count(total, min_tiles, max_slices, quantum);
   for (int s = tid; s <= n; s += kPlanThreads) {
     SliceStart st;
     if (s == n) {
@@ -169,10 +169,10 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
-                       int32_t max_slices, int32_t min_tiles, PlanHeader* hdr,
+                       int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* hdr,
                        SliceStart* starts, int32_t* prefix, hipStream_t stream) {
-  plan_kernel<<<1, kPlanThreads, 0, stream>>>(lens, batch, hkv, mbps, max_slices, min_tiles, hdr,
-                                              starts, prefix);
+  plan_kernel<<<1, kPlanThreads, 0, stream>>>(lens, batch, hkv, mbps, max_slices, min_tiles,
+                                              quantum, hdr, starts, prefix);
   return hipGetLastError();
 }
 

@@ -332,3 +332,19 @@ def test_binding_errors_are_raised():
     assert ei.value.status == 3
     with pytest.raises(neo.NeoError):
         neo.decode_attention(q, k, v, bt, sl, scale=math.inf)
+
+
+def test_matches_golden_fixture():
+    import json
+    import os
+    here = os.path.dirname(os.path.abspath(__file__))
+    rec = json.load(open(os.path.join(here, "golden", "oracle_small.json")))
+    s = rec["spec"]
+    case = W.build_case(s["seq_lens"], s["num_q_heads"], s["num_kv_heads"], s["head_dim"],
+                        s["block_size"], seed=s["seed"])
+    expect = np.array([[[float.fromhex(x) for x in row] for row in head]
+                       for head in rec["out_f32_hex"]], dtype=np.float32)
+    for variant in ("valu", "mfma"):
+        for schedule in ("staged", "fused"):
+            assert_parity(run(case, variant=variant, schedule=schedule), expect,
+                          f"golden {variant} {schedule}")

@@ -337,3 +337,18 @@ def test_config_lengths_follow_recipes():
     L5 = W.config_seq_lens(5, 5)
     assert L5.shape == (1024,) and int((L5 == 32768).sum()) == 8
     assert L5[L5 != 32768].max() <= 256 and L5.min() >= 16
+
+
+# ----------------------------------------------------------------- regression fixture
+
+def test_oracle_reproduces_golden_fixture():
+    import json
+    import os
+    here = os.path.dirname(os.path.abspath(__file__))
+    rec = json.load(open(os.path.join(here, "golden", "oracle_small.json")))
+    s = rec["spec"]
+    case = W.build_case(s["seq_lens"], s["num_q_heads"], s["num_kv_heads"], s["head_dim"],
+                        s["block_size"], seed=s["seed"])
+    expect = np.array([[[float.fromhex(x) for x in row] for row in head]
+                       for head in rec["out_f32_hex"]], dtype=np.float32)
+    assert np.array_equal(oracle.decode_attention(case), expect)
