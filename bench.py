@@ -139,7 +139,8 @@ def main(argv=None):
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--variant", default="auto", choices=["auto", "valu", "mfma"])
-    ap.add_argument("--schedule", default="auto", choices=["auto", "fused", "staged"])
+    ap.add_argument("--schedule", default="auto",
+                    choices=["auto", "fused", "staged", "two_kernel"])
     ap.add_argument("--max-slices", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -175,7 +176,7 @@ def main(argv=None):
     sh = ctypes.c_void_p(stream.cuda_stream)
     variant_id = neo.VARIANTS[args.variant]
     schedule_id = neo.SCHEDULES[args.schedule]
-    schedule = "fused" if args.schedule == "fused" else "staged"
+    schedule = "two_kernel" if args.schedule == "auto" else args.schedule
     resolved = "mfma" if args.variant == "auto" else args.variant
     hip = HipEvents()
     ev = [(hip.create(), hip.create()) for _ in range(args.steps)]
@@ -255,7 +256,7 @@ def main(argv=None):
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": f"decode_{resolved}_kernel<{case.group}, {schedule == 'fused'}>",
+            "kernel": f"decode_{resolved}_kernel<{case.group}, {schedule}>",
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

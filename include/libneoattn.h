@@ -79,10 +79,11 @@ typedef enum {
 
 /* How the call is launched (neo_decode_attention_ex). */
 typedef enum {
-  NEO_SCHEDULE_AUTO = 0,   /* staged (the faster on MI355X for most length mixes) */
-  NEO_SCHEDULE_FUSED = 1,  /* one kernel: each wavefront plans its own slice from seq_lens and
-                              the last slice to finish a split request merges it */
-  NEO_SCHEDULE_STAGED = 2  /* three kernels: plan, decode, log-sum-exp combine */
+  NEO_SCHEDULE_AUTO = 0,       /* two-kernel (the fastest on MI355X for every length mix tried) */
+  NEO_SCHEDULE_FUSED = 1,      /* one kernel: each wavefront plans its own slice from seq_lens
+                                  and the last slice to finish a split request merges it */
+  NEO_SCHEDULE_STAGED = 2,     /* three kernels: plan, decode, log-sum-exp combine */
+  NEO_SCHEDULE_TWO_KERNEL = 3  /* decode (planning in-wave, recording the plan), then combine */
 } neo_schedule;
 
 /* Largest number of sequence slices (one wavefront each) a call may use. */
@@ -110,7 +111,7 @@ neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, vo
  * The first eleven arguments follow the problem statement in that order; the rest
  * are what a device pointer cannot carry: batch size, block-table row stride
  * (max_blocks_per_seq), pool size (num_blocks), the workspace and the stream.
- * Enqueues three kernels (the staged schedule). Reads q, k_cache, v_cache,
+ * Enqueues two kernels (decode, combine). Reads q, k_cache, v_cache,
  * block_table and seq_lens; writes out and the workspace.
  * batch == 0 is a no-op (pointers may then be NULL).
  */

@@ -34,7 +34,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libneoattn.so")
 
 VARIANTS = {"auto": 0, "valu": 1, "mfma": 2}
-SCHEDULES = {"auto": 0, "fused": 1, "staged": 2}
+SCHEDULES = {"auto": 0, "fused": 1, "staged": 2, "two_kernel": 3}
 MAX_SLICES = 4096
 STATUS = {0: "NEO_OK", 1: "NEO_ERR_INVALID_ARG", 2: "NEO_ERR_UNSUPPORTED",
           3: "NEO_ERR_WORKSPACE", 4: "NEO_ERR_HIP"}
@@ -167,8 +167,9 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
     """Decode attention of the whole ragged batch; returns ``out`` (fp32 [B, Hq, 128]).
 
     ``scale`` defaults to 1/sqrt(head_dim). ``variant`` picks the kernel family
-    ("auto", "valu", "mfma"); ``schedule`` the launch ("auto"/"staged": plan,
-    decode and combine kernels; "fused": one kernel); ``max_slices`` caps
+    ("auto", "valu", "mfma"); ``schedule`` the launch ("auto"/"two_kernel":
+    decode then combine; "staged": plan, decode and combine; "fused": one
+    kernel); ``max_slices`` caps
     the sequence slices of the plan (0 = library default, 1 = never split a
     request). ``workspace`` (a zero-filled uint8 GPU tensor of at least
     ``workspace_bytes(...)``, see ``new_workspace``) is allocated and cached per

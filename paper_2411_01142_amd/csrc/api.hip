@@ -113,7 +113,7 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
     return fail(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
   if (schedule != NEO_SCHEDULE_AUTO && schedule != NEO_SCHEDULE_FUSED &&
-      schedule != NEO_SCHEDULE_STAGED)
+      schedule != NEO_SCHEDULE_STAGED && schedule != NEO_SCHEDULE_TWO_KERNEL)
     return fail(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
   if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
     return fail(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
@@ -124,9 +124,9 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
     return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
                 max_blocks_per_seq, num_blocks);
-  if ((int64_t)batch * max_blocks_per_seq * num_kv_heads >= ((int64_t)1 << 31))
+  if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCost) * num_kv_heads >= ((int64_t)1 << 31))
     return fail(NEO_ERR_INVALID_ARG,
-                "batch * max_blocks_per_seq * num_kv_heads must stay below 2^31");
+                "batch * (max_blocks_per_seq + 2) * num_kv_heads must stay below 2^31");
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
     return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
@@ -149,10 +149,12 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
       max_slices == 0 ? std::min<int32_t>(2 * quantum, NEO_MAX_SLICES) : max_slices;
   const int32_t min_tiles = max_slices == 0 ? 0 : 1;
   if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
-  // Staged by default: measured on MI355X it is as fast or faster than the
-  // fused launch on every workload shape but the most skewed one, because
-  // three short launches cost less than the fused kernel's in-kernel merges.
-  const bool fused = schedule == NEO_SCHEDULE_FUSED;
+  // Default: decode (planning in-wave) + combine. Measured on MI355X it beats
+  // the three-kernel launch (one launch and one plan read fewer) and the fused
+  // kernel (whose in-kernel merges cost more than a short combine launch).
+  const neo::Schedule sched = schedule == NEO_SCHEDULE_FUSED    ? neo::kFused
+                              : schedule == NEO_SCHEDULE_STAGED ? neo::kStaged
+                                                                : neo::kTwoKernel;
 
   char* ws = static_cast<char*>(workspace);
   neo::DecodeParams p;
@@ -162,8 +164,8 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   p.table = block_table;
   p.lens = seq_lens;
   p.out = out;
-  p.hdr = reinterpret_cast<const neo::PlanHeader*>(ws + wl.hdr);
-  p.starts = reinterpret_cast<const neo::SliceStart*>(ws + wl.starts);
+  p.hdr = reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr);
+  p.starts = reinterpret_cast<neo::SliceStart*>(ws + wl.starts);
   p.part_lse = reinterpret_cast<float*>(ws + wl.part_lse);
   p.part_o = reinterpret_cast<float*>(ws + wl.part_o);
   p.counters = reinterpret_cast<int32_t*>(ws + wl.counters);
@@ -179,7 +181,7 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
-  if (!fused) {
+  if (sched == neo::kStaged) {
     e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices, min_tiles,
                          quantum, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
                          reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
@@ -191,14 +193,14 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
     e = hipEventRecord(static_cast<hipEvent_t>(decode_start_event), s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
-  e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, fused, grid, s)
-                                  : neo::launch_decode_mfma(p, group, fused, grid, s);
+  e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, sched, grid, s)
+                                  : neo::launch_decode_mfma(p, group, sched, grid, s);
   if (e != hipSuccess) return fail(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   if (decode_end_event) {
     e = hipEventRecord(static_cast<hipEvent_t>(decode_end_event), s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
-  if (!fused) {
+  if (sched != neo::kFused) {
     e = neo::launch_combine(p, group, grid, s);
     if (e != hipSuccess) return fail(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
   }

@@ -1,14 +1,17 @@
 // The decode driver shared by both kernel families: how a wavefront finds its
-// slice of the batch, walks (request, kv head, block) tiles with loads
-// issued ahead of use, and where a finished segment's result goes (straight
-// to `out`, or to a partial slot that the last contributor merges).
+// slice of the batch, walks (request, kv head, block) tiles with loads issued
+// ahead of use, and where a finished segment's result goes (straight to `out`,
+// or to a partial slot that is merged afterwards).
 //
-// Tiles are numbered request-major, kv-head-next, block-minor; with T tiles
-// and n slices, slice s owns [floor(sT/n), floor((s+1)T/n)). A (request, kv
-// head) pair whose tiles cross a slice boundary is "cut": every slice that
-// touches it writes a partial output normalised over its share plus the
-// log-sum-exp of its scores, and the pair is aggregated afterwards (the
-// block-granular split and per-request aggregation of Sec. 4 of the paper).
+// Work is balanced on a weighted line: each (request, kv head) pair with nb > 0
+// blocks occupies nb + kPairCost positions, its startup cost (q, block ids,
+// pipeline fill) followed by one position per block tile. With W positions in
+// all and n slices, slice s owns [floor(sW/n), floor((s+1)W/n)) and processes
+// the tiles whose positions fall there. A pair whose tiles cross a slice
+// boundary is "cut": every slice holding some of its tiles writes a partial
+// output normalised over its share plus the log-sum-exp of its scores, and the
+// pair is aggregated afterwards (the block-granular split and per-request
+// aggregation of Sec. 4 of the paper).
 #pragma once
 
 #include <math.h>
@@ -47,42 +50,44 @@ __device__ inline void wait_all_memory() {
 
 // ----------------------------------------------------------------- slice geometry
 
-__device__ inline int32_t slice_first_tile(int64_t s, int32_t T, int32_t n) {
-  return (int32_t)((s * T) / n);
+__device__ inline int32_t slice_start(int64_t s, int32_t W, int32_t n) {
+  return (int32_t)((s * W) / n);
 }
-// The slice holding tile t: the largest s with floor(sT/n) <= t.
-__device__ inline int32_t slice_of_tile(int32_t t, int32_t T, int32_t n) {
-  return (int32_t)((((int64_t)t + 1) * n - 1) / T);
+// The slice holding position x: the largest s with floor(sW/n) <= x.
+__device__ inline int32_t slice_of(int32_t x, int32_t W, int32_t n) {
+  return (int32_t)((((int64_t)x + 1) * n - 1) / W);
 }
-// Partial slot of slice w for a pair starting at tile pair_first: a slice's
-// first segment uses 2w, a later (end-cut) segment 2w+1. At most one of each.
-__device__ inline int partial_slot(int32_t w, int32_t slice_first, int32_t pair_first) {
-  return slice_first >= pair_first ? 2 * w : 2 * w + 1;
+// Partial slot of slice s for a pair whose first tile sits at position
+// first_tile: 2s when that tile is at or before the slice start (the pair runs
+// into the slice: its first segment), else 2s+1 (a pair starting inside the
+// slice and cut by its end). A slice has at most one of each.
+__device__ inline int partial_slot(int32_t s, int32_t slice_first, int32_t first_tile) {
+  return first_tile <= slice_first ? 2 * s : 2 * s + 1;
 }
 
-// Number of slices for T tiles. With min_tiles > 0: T / min_tiles, capped.
+// Number of slices for W positions. With min_tiles > 0: W / min_tiles, capped.
 // With min_tiles == 0 (the default policy): whole multiples of `quantum` (one
 // 4-wave workgroup per CU) so every CU gets the same share, stepping up to
-// two workgroups per CU once slices still hold kAutoTilesPerSlice tiles;
-// small batches get T / 8 slices.
+// two workgroups per CU once slices still hold kAutoTilesPerSlice positions;
+// small batches get W / 8 slices.
 constexpr int32_t kAutoTilesPerSlice = 40;
 constexpr int32_t kSmallTilesPerSlice = 8;
 
-__device__ inline int32_t slice_count(int32_t T, int32_t min_tiles, int32_t max_slices,
-                                      int32_t quantum) {
-  if (T <= 0) return 0;
-  if (min_tiles > 0) return min(max(T / min_tiles, 1), max_slices);
+__host__ __device__ inline int32_t slice_count(int32_t W, int32_t min_tiles, int32_t max_slices,
+                                               int32_t quantum) {
+  if (W <= 0) return 0;
+  if (min_tiles > 0) return min(max(W / min_tiles, 1), max_slices);
   int32_t n;
-  if (T >= 2 * quantum * kAutoTilesPerSlice) n = 2 * quantum;
-  else if (T >= quantum * kSmallTilesPerSlice) n = quantum;
-  else n = max(T / kSmallTilesPerSlice, 1);
+  if (W >= 2 * quantum * kAutoTilesPerSlice) n = 2 * quantum;
+  else if (W >= quantum * kSmallTilesPerSlice) n = quantum;
+  else n = max(W / kSmallTilesPerSlice, 1);
   return min(n, max_slices);
 }
 
 struct SliceInfo {
-  int32_t T, n;      // total tiles, slices
-  int32_t s0, s1;    // this slice's tile range
-  int32_t b, g, j;   // coordinates of tile s0
+  int32_t W, n;      // total positions, slices
+  int32_t s0, s1;    // this slice's position range
+  int32_t b, g, x;   // pair holding position s0 and the offset of s0 inside it
 };
 
 // ----------------------------------------------------------------- wave helpers
@@ -116,80 +121,80 @@ __device__ inline int32_t wave_incl_scan_i32(int32_t v, int lane) {
 // Slice from the plan kernel's output (staged launch).
 __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
   SliceInfo si;
-  si.T = p.hdr->total_tiles;
+  si.W = p.hdr->total;
   si.n = p.hdr->n_slices;
   if (wave >= si.n) return si;
   const SliceStart a = p.starts[wave];
-  si.s0 = a.tile;
-  si.s1 = p.starts[wave + 1].tile;
+  si.s0 = a.pos;
+  si.s1 = p.starts[wave + 1].pos;
   si.b = a.b;
   si.g = a.g;
-  si.j = a.j;
+  si.x = a.x;
   return si;
 }
 
 // Slice computed by the wavefront itself from seq_lens (fused launch): a
-// wave-wide reduction of the block counts gives T; a wave-wide scan locates
-// the request holding the slice's first tile. Requests are read 64 per lane
-// group, up to kPlanRegs groups per load round.
+// wave-wide reduction of the request weights gives W; a wave-wide scan locates
+// the request holding the slice's first position. Requests are read 64 per
+// lane group, up to kPlanRegs groups per load round.
 constexpr int kPlanRegs = 16;
 
-// Block counts of requests base + 64r + lane, r < kPlanRegs (0 past the batch).
+// Weights of requests base + 64r + lane, r < kPlanRegs (0 past the batch).
 // Loads use a clamped index so that all of them issue before any is waited on.
-__device__ inline void load_block_counts(const DecodeParams& p, int base, int lane,
-                                         int32_t (&nb)[kPlanRegs]) {
+__device__ inline void load_weights(const DecodeParams& p, int base, int lane,
+                                    int32_t (&w)[kPlanRegs]) {
   int32_t raw[kPlanRegs];
 #pragma unroll
   for (int r = 0; r < kPlanRegs; ++r) raw[r] = p.lens[min(base + r * kWave + lane, p.batch - 1)];
 #pragma unroll
   for (int r = 0; r < kPlanRegs; ++r)
-    nb[r] = (base + r * kWave + lane < p.batch) ? blocks_of(raw[r], p.mbps) : 0;
+    w[r] = (base + r * kWave + lane < p.batch) ? pair_weight(raw[r], p.mbps) : 0;
 }
 
 __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int lane) {
   SliceInfo si;
   constexpr int kChunk = kWave * kPlanRegs;
-  int32_t nb[kPlanRegs];
+  int32_t w[kPlanRegs];
   int32_t total = 0;
   for (int base = 0; base < p.batch; base += kChunk) {
-    load_block_counts(p, base, lane, nb);
+    load_weights(p, base, lane, w);
     int32_t s = 0;
 #pragma unroll
-    for (int r = 0; r < kPlanRegs; ++r) s += nb[r];
+    for (int r = 0; r < kPlanRegs; ++r) s += w[r];
     total += wave_sum_i32(s);
   }
-  si.T = total * p.hkv;
-  si.n = slice_count(si.T, p.min_tiles, p.max_slices, p.slice_quantum);
+  si.W = total * p.hkv;
+  si.n = slice_count(si.W, p.min_tiles, p.max_slices, p.slice_quantum);
   if (wave >= si.n) return si;
-  si.s0 = slice_first_tile(wave, si.T, si.n);
-  si.s1 = slice_first_tile((int64_t)wave + 1, si.T, si.n);
+  si.s0 = slice_start(wave, si.W, si.n);
+  si.s1 = slice_start((int64_t)wave + 1, si.W, si.n);
 
-  // Request b holds tiles [hkv*P_b, hkv*P_{b+1}) with P the block prefix sum.
+  // Request b holds positions [hkv*P_b, hkv*P_{b+1}) with P the weight prefix sum.
   const int32_t u = si.s0 / p.hkv;
   int32_t carry = 0;
   int32_t found_b = -1, found_p = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
-    if (p.batch > kChunk) load_block_counts(p, base, lane, nb);
+    if (p.batch > kChunk) load_weights(p, base, lane, w);
 #pragma unroll
     for (int r = 0; r < kPlanRegs; ++r) {
       if (found_b >= 0) break;
-      const int32_t cs = wave_sum_i32(nb[r]);
+      const int32_t cs = wave_sum_i32(w[r]);
       if (carry + cs > u) {
-        const int32_t incl = wave_incl_scan_i32(nb[r], lane);
+        const int32_t incl = wave_incl_scan_i32(w[r], lane);
         const uint64_t hit = __ballot(carry + incl > u);
         const int first = __ffsll((unsigned long long)hit) - 1;
         found_b = base + r * kWave + first;
-        found_p = carry + __shfl(incl - nb[r], first);
+        found_p = carry + __shfl(incl - w[r], first);
       } else {
         carry += cs;
       }
     }
   }
-  const int32_t nbb = blocks_of(p.lens[found_b], p.mbps);
+  const int32_t wb = pair_weight(p.lens[found_b], p.mbps);
   const int32_t rem = si.s0 - p.hkv * found_p;
   si.b = found_b;
-  si.g = rem / nbb;
-  si.j = rem % nbb;
+  si.g = rem / wb;
+  si.x = rem % wb;
   return si;
 }
 
@@ -205,58 +210,65 @@ __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwav
   }
 }
 
-// Merge the partials of one cut pair into out[b][g*G .. g*G+G): M = max lse,
-// out = sum_c e^(lse_c - M) o_c / sum_c e^(lse_c - M). Contributors are the
-// slices c0..c1. Each lane owns dims 2*lane, 2*lane+1 of the sums.
-template <int G>
-__device__ inline int contributor_slot(int32_t c, int32_t T, int32_t n, int32_t pair_first) {
-  return partial_slot(c, slice_first_tile(c, T, n), pair_first);
-}
-
-template <int G>
-__device__ inline void store_merged(const DecodeParams& p, int32_t b, int32_t g, int h, int d,
-                                    float a0, float a1, float z) {
-  const float inv = 1.f / z;
-  float2 r;
-  r.x = a0 * inv;
-  r.y = a1 * inv;
-  *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
-}
-
-template <int G>
-__device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, int32_t pair_first,
-                                  int32_t c0, int32_t c1, int32_t T, int32_t n, int lane) {
+// Merge the partials of one cut pair into out[b][g*G .. g*G+G): with M the
+// largest log-sum-exp, out = sum_c e^(lse_c - M) o_c / sum_c e^(lse_c - M).
+// Contributors are slices c0..c1, taken 64 at a time with a running maximum
+// (earlier sums are rescaled when it grows). Lane i reads the log-sum-exps of
+// contributor i of the chunk; each lane owns dims 2*lane, 2*lane+1 of the
+// sums; partial rows are read kBatch contributors at a time, the first batch
+// issued together with the log-sum-exps. kCoherent: the partials were written
+// by other wavefronts of the running kernel.
+template <int G, bool kCoherent>
+__device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, int32_t first_tile,
+                                  int32_t c0, int32_t c1, int32_t W, int32_t n, int lane) {
+  constexpr int kBatch = 32 / G > 16 ? 16 : (32 / G > 0 ? 32 / G : 1);  // 64 registers
+  auto ld = [](const float* a) -> float { return kCoherent ? load_coherent(a) : *a; };
   const int k = c1 - c0 + 1;
   const int d = 2 * lane;
-  if (k <= kWave) {
-    // Lane i reads the log-sum-exps of contributor c0 + i; partial rows are
-    // then read kBatch contributors at a time with all loads issued together.
-    constexpr int kBatch = 32 / G > 16 ? 16 : (32 / G > 0 ? 32 / G : 1);  // 64 registers
-    const int mine = lane < k ? lane : 0;
-    const int my_slot = contributor_slot<G>(c0 + mine, T, n, pair_first);
-    float w[G], a0[G], a1[G];
+  float m[G], z[G], a0[G], a1[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float lse = lane < k ? load_coherent(p.part_lse + my_slot * G + h) : -INFINITY;
-      w[h] = __expf(lse - wave_max_f32(lse));
-      a0[h] = a1[h] = 0.f;
-    }
-    for (int i0 = 0; i0 < k; i0 += kBatch) {
-      float ov[kBatch][G][2];
+  for (int h = 0; h < G; ++h) {
+    m[h] = -INFINITY;
+    z[h] = a0[h] = a1[h] = 0.f;
+  }
+  for (int base = 0; base < k; base += kWave) {
+    const int cnt = min(kWave, k - base);
+    float ov[kBatch][G][2];
+    auto load_rows = [&](int i0, bool clamp) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        if (i0 + u >= k) break;  // uniform
-        const int slot = contributor_slot<G>(c0 + i0 + u, T, n, pair_first);
+        if (!clamp && i0 + u >= cnt) break;  // uniform
+        const int c = c0 + base + min(i0 + u, cnt - 1);
+        const int slot = partial_slot(c, slice_start(c, W, n), first_tile);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
-          ov[u][h][0] = load_coherent(o);
-          ov[u][h][1] = load_coherent(o + 1);
+          ov[u][h][0] = ld(o);
+          ov[u][h][1] = ld(o + 1);
         }
       }
+    };
+    load_rows(0, true);
+    const int mine = c0 + base + (lane < cnt ? lane : 0);
+    const int my_slot = partial_slot(mine, slice_start(mine, W, n), first_tile);
+    float w[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float lse = lane < cnt ? ld(p.part_lse + my_slot * G + h) : -INFINITY;
+      const float mc = fmaxf(m[h], wave_max_f32(lse));
+      const float rescale = __expf(m[h] - mc);  // 0 on the first chunk
+      a0[h] *= rescale;
+      a1[h] *= rescale;
+      z[h] *= rescale;
+      m[h] = mc;
+      w[h] = __expf(lse - mc);
+      z[h] += wave_sum_f32(w[h]);
+    }
+    for (int i0 = 0; i0 < cnt; i0 += kBatch) {
+      if (i0 > 0) load_rows(i0, false);
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        if (i0 + u >= k) break;
+        if (i0 + u >= cnt) break;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           const float wi = __shfl(w[h], i0 + u);
@@ -265,40 +277,21 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
         }
       }
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h) store_merged<G>(p, b, g, h, d, a0[h], a1[h], wave_sum_f32(w[h]));
-    return;
   }
-  // More than 64 contributors (a very long request cut into many slices):
-  // global maximum first, then the weighted sums, one contributor at a time.
+#pragma unroll
   for (int h = 0; h < G; ++h) {
-    float m = -INFINITY;
-    for (int base = 0; base < k; base += kWave)
-      if (base + lane < k)
-        m = fmaxf(m, load_coherent(p.part_lse +
-                                   contributor_slot<G>(c0 + base + lane, T, n, pair_first) * G +
-                                   h));
-    m = wave_max_f32(m);
-    float z = 0.f, a0 = 0.f, a1 = 0.f;
-    for (int i = 0; i < k; ++i) {
-      const int slot = contributor_slot<G>(c0 + i, T, n, pair_first);
-      const float wi = __expf(load_coherent(p.part_lse + slot * G + h) - m);
-      const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
-      z += wi;
-      a0 = fmaf(wi, load_coherent(o), a0);
-      a1 = fmaf(wi, load_coherent(o + 1), a1);
-    }
-    store_merged<G>(p, b, g, h, d, a0, a1, z);
+    const float inv = 1.f / z[h];
+    float2 r;
+    r.x = a0[h] * inv;
+    r.y = a1[h] * inv;
+    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
   }
 }
 
 // Fused launch: after writing its partial for a cut pair, a slice counts itself
 // in the pair's counter; the slice that completes the count merges the pair
 // (returns true) and resets the counter to zero for the next call.
-__device__ inline bool arrive_last(const DecodeParams& p, int32_t pair_first, int32_t pair_tiles,
-                                   int32_t T, int32_t n, int lane) {
-  const int32_t c0 = slice_of_tile(pair_first, T, n);
-  const int32_t c1 = slice_of_tile(pair_first + pair_tiles - 1, T, n);
+__device__ inline bool arrive_last(const DecodeParams& p, int32_t c0, int32_t c1, int lane) {
   wait_all_memory();  // this slice's partial has reached the coherence point
   int32_t old = 0;
   if (lane == 0)
@@ -312,16 +305,44 @@ __device__ inline bool arrive_last(const DecodeParams& p, int32_t pair_first, in
 
 // ----------------------------------------------------------------- the driver
 
-// Family provides: Tile, State, Q; load_q, init, load_tile, step, write.
+// Family provides: Tile, State, Q, Shared; load_q, init, load_tile, step, write.
 // PF tiles are in flight ahead of the one being computed.
-template <class F, int G, int PF, bool kFused>
+template <class F, int G, int PF, Schedule kSched>
 __device__ inline void decode_driver(const DecodeParams& p) {
+  constexpr bool kMergeHere = kSched == kFused;  // merge cut pairs in this kernel
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x >> 6;
   const int wave = blockIdx.x * kWavesPerGroup + wv;
   const int nwaves = gridDim.x * kWavesPerGroup;
   zero_empty_rows(p, wave, nwaves, lane);
-  const SliceInfo si = kFused ? plan_in_wave(p, wave, lane) : read_plan(p, wave);
+  const SliceInfo si = kSched == kStaged ? read_plan(p, wave) : plan_in_wave(p, wave, lane);
+  if (kSched == kTwoKernel && lane == 0) {
+    // Record the plan for the combine kernel.
+    if (wave < si.n) {
+      SliceStart a;
+      a.pos = si.s0;
+      a.b = si.b;
+      a.g = si.g;
+      a.x = si.x;
+      a.nb = blocks_of(p.lens[si.b], p.mbps);
+      a.pad[0] = a.pad[1] = a.pad[2] = 0;
+      p.starts[wave] = a;
+    }
+    if (wave == 0) {
+      SliceStart e;
+      e.pos = si.W;
+      e.b = p.batch;
+      e.g = e.x = e.nb = 0;
+      e.pad[0] = e.pad[1] = e.pad[2] = 0;
+      p.starts[si.n] = e;
+      PlanHeader h;
+      h.total = si.W;
+      h.n_slices = si.n;
+      h.batch = p.batch;
+      h.pad = 0;
+      *p.hdr = h;
+    }
+  }
   if (wave >= si.n) return;
 
   __shared__ typename F::Shared shared[kWavesPerGroup];
@@ -329,25 +350,29 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   const size_t blk_stride = (size_t)p.hkv * kTileElems;
 
   // A slice holds at most two cut pairs: the one it starts in and the one it
-  // ends in.
+  // ends in. Their merges (fused launch) run after the tile loop.
   struct Pending {
-    int32_t b, g, first, tiles;
+    int32_t b, g, first, c0, c1;
   } pend[2];
   int npend = 0;
 
-  int32_t t = si.s0;
-  int b = si.b, g = si.g, j = si.j;
-  while (t < si.s1 && b < p.batch) {
+  int32_t pos = si.s0;  // weighted position reached
+  int b = si.b, g = si.g;
+  int32_t x = si.x;     // offset of pos inside pair (b, g)
+  while (b < p.batch) {
     const int32_t L = clamp_len(p.lens[b], p.mbps);
     const int32_t nb = (L + kBlock - 1) / kBlock;
     if (nb == 0) {
       ++b;
       g = 0;
-      j = 0;
+      x = 0;
       continue;
     }
-    const int32_t jend = min(nb, j + (si.s1 - t));
-    const int32_t pair_first = t - j;
+    const int32_t pair_base = pos - x;
+    const int32_t first_tile = pair_base + kPairCost;  // position of block 0
+    const int32_t j = max(0, x - kPairCost);
+    const int32_t jend = min(nb, si.s1 - first_tile);
+    if (jend <= j) break;  // the slice ends before this pair's next tile
 
     // Block ids of this row, 64 at a time, one per lane.
     const int32_t* trow = p.table + (size_t)b * p.mbps;
@@ -392,35 +417,35 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     if (j == 0 && jend == nb) {
       F::template write<false>(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);
     } else {
-      const int slot = partial_slot(wave, si.s0, pair_first);
-      F::template write<true>(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
-                              lane);
-      if (kFused && arrive_last(p, pair_first, nb, si.T, si.n, lane)) {
-        // Merge after the tile loop, when the tile buffers are no longer live.
-        pend[npend].b = b;
-        pend[npend].g = g;
-        pend[npend].first = pair_first;
-        pend[npend].tiles = nb;
-        ++npend;
+      const int slot = partial_slot(wave, si.s0, first_tile);
+      F::template write<kMergeHere>(st, p.part_o + (size_t)slot * G * kHeadDim,
+                                p.part_lse + slot * G, lane);
+      if (kMergeHere) {
+        const int32_t c0 = slice_of(first_tile, si.W, si.n);
+        const int32_t c1 = slice_of(first_tile + nb - 1, si.W, si.n);
+        if (arrive_last(p, c0, c1, lane)) {
+          pend[npend].b = b;
+          pend[npend].g = g;
+          pend[npend].first = first_tile;
+          pend[npend].c0 = c0;
+          pend[npend].c1 = c1;
+          ++npend;
+        }
       }
     }
 
-    t += jend - j;
-    j = jend;
-    if (j == nb) {
-      j = 0;
-      if (++g == p.hkv) {
-        g = 0;
-        ++b;
-      }
+    pos = pair_base + nb + kPairCost;
+    x = 0;
+    if (pos >= si.s1) break;
+    if (++g == p.hkv) {
+      g = 0;
+      ++b;
     }
   }
-  if (kFused) {
-    for (int i = 0; i < npend; ++i) {
-      const int32_t c0 = slice_of_tile(pend[i].first, si.T, si.n);
-      const int32_t c1 = slice_of_tile(pend[i].first + pend[i].tiles - 1, si.T, si.n);
-      merge_pair<G>(p, pend[i].b, pend[i].g, pend[i].first, c0, c1, si.T, si.n, lane);
-    }
+  if (kMergeHere) {
+    for (int i = 0; i < npend; ++i)
+      merge_pair<G, true>(p, pend[i].b, pend[i].g, pend[i].first, pend[i].c0, pend[i].c1, si.W,
+                          si.n, lane);
   }
 }
 

@@ -190,31 +190,32 @@ struct ValuFamily {
   }
 };
 
-template <int G, bool kFused>
+template <int G, Schedule kSched>
 __global__ __launch_bounds__(kWave * kWavesPerGroup) void decode_valu_kernel(DecodeParams p) {
-  decode_driver<ValuFamily<G>, G, 1, kFused>(p);
+  decode_driver<ValuFamily<G>, G, 1, kSched>(p);
 }
 
 template <int G>
-hipError_t launch_g(const DecodeParams& p, bool fused, int32_t grid, hipStream_t stream) {
+hipError_t launch_g(const DecodeParams& p, Schedule sched, int32_t grid, hipStream_t stream) {
   const dim3 block(kWave * kWavesPerGroup);
-  if (fused)
-    decode_valu_kernel<G, true><<<grid, block, 0, stream>>>(p);
-  else
-    decode_valu_kernel<G, false><<<grid, block, 0, stream>>>(p);
+  switch (sched) {
+    case kStaged: decode_valu_kernel<G, kStaged><<<grid, block, 0, stream>>>(p); break;
+    case kFused: decode_valu_kernel<G, kFused><<<grid, block, 0, stream>>>(p); break;
+    case kTwoKernel: decode_valu_kernel<G, kTwoKernel><<<grid, block, 0, stream>>>(p); break;
+  }
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
-                              hipStream_t stream) {
+hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, Schedule sched,
+                              int32_t grid, hipStream_t stream) {
   switch (group) {
-    case 1: return launch_g<1>(p, fused, grid, stream);
-    case 2: return launch_g<2>(p, fused, grid, stream);
-    case 4: return launch_g<4>(p, fused, grid, stream);
-    case 8: return launch_g<8>(p, fused, grid, stream);
-    case 16: return launch_g<16>(p, fused, grid, stream);
+    case 1: return launch_g<1>(p, sched, grid, stream);
+    case 2: return launch_g<2>(p, sched, grid, stream);
+    case 4: return launch_g<4>(p, sched, grid, stream);
+    case 8: return launch_g<8>(p, sched, grid, stream);
+    case 16: return launch_g<16>(p, sched, grid, stream);
     default: return hipErrorInvalidValue;
   }
 }

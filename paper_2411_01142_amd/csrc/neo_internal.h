@@ -18,22 +18,32 @@ constexpr int kWave = 64;
 constexpr int kWavesPerGroup = 4;               // wavefronts per workgroup (256 threads)
 constexpr int kPlanThreads = 1024;
 
-// Work plan. The batch's (request, kv head, block) tiles are numbered in
-// request-major, kv-head-next, block-minor order; slice s owns the contiguous
-// tile range [starts[s].tile, starts[s+1].tile) and is run by one wavefront.
+// Work plan. Each (request, kv head) pair with nb > 0 blocks occupies
+// nb + kPairCost positions of a weighted line (its startup cost, then one
+// position per block tile), pairs in request-major, kv-head-next order; slice
+// s owns positions [starts[s].pos, starts[s+1].pos) and is run by one
+// wavefront.
+constexpr int32_t kPairCost = 2;
+
 struct alignas(16) PlanHeader {
-  int32_t total_tiles;
+  int32_t total;     // positions on the weighted line
   int32_t n_slices;
   int32_t batch;
   int32_t pad;
 };
 
-struct alignas(16) SliceStart {
-  int32_t tile;  // first flat tile of the slice
-  int32_t b;     // its request
-  int32_t g;     // its kv head
-  int32_t j;     // its block index inside the request
+struct alignas(32) SliceStart {
+  int32_t pos;  // first position of the slice
+  int32_t b;    // request of the pair holding it
+  int32_t g;    // kv head of that pair
+  int32_t x;    // offset of pos inside the pair's nb + kPairCost positions
+  int32_t nb;   // blocks of that pair
+  int32_t pad[3];
 };
+
+// Launch schedules: plan kernel + decode + combine kernel; one fused kernel;
+// decode (planning in-wave, recording slice starts) + combine kernel.
+enum Schedule { kStaged = 0, kFused = 1, kTwoKernel = 2 };
 
 struct WorkspaceLayout {
   size_t hdr, starts, counters, prefix, part_lse, part_o, total;
@@ -71,6 +81,11 @@ __host__ __device__ inline int32_t clamp_len(int32_t L, int32_t mbps) {
 __host__ __device__ inline int32_t blocks_of(int32_t L, int32_t mbps) {
   return (clamp_len(L, mbps) + kBlock - 1) / kBlock;
 }
+// Positions of each (request, kv head) pair of a request with this length.
+__host__ __device__ inline int32_t pair_weight(int32_t L, int32_t mbps) {
+  const int32_t nb = blocks_of(L, mbps);
+  return nb > 0 ? nb + kPairCost : 0;
+}
 
 struct DecodeParams {
   const uint16_t* q;          // [batch][hq][128] bf16
@@ -79,8 +94,8 @@ struct DecodeParams {
   const int32_t* table;       // [batch][mbps]
   const int32_t* lens;        // [batch]
   float* out;                 // [batch][hq][128]
-  const PlanHeader* hdr;
-  const SliceStart* starts;
+  PlanHeader* hdr;
+  SliceStart* starts;
   float* part_lse;            // [2*NEO_MAX_SLICES][group]
   float* part_o;              // [2*NEO_MAX_SLICES][group][128]
   int32_t* counters;          // [NEO_MAX_SLICES]
@@ -94,10 +109,10 @@ struct DecodeParams {
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
                        int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* hdr,
                        SliceStart* starts, int32_t* prefix, hipStream_t stream);
-hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
-                              hipStream_t stream);
-hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, bool fused, int32_t grid,
-                              hipStream_t stream);
+hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, Schedule sched,
+                              int32_t grid, hipStream_t stream);
+hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, Schedule sched,
+                              int32_t grid, hipStream_t stream);
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hipStream_t stream);
 hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,

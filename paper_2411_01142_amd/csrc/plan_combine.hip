@@ -14,9 +14,9 @@
 namespace neo {
 namespace {
 
-// One workgroup: block counts, an exclusive scan over requests (tile
-// offsets), then each slice's first tile located by binary search (over an
-// LDS copy of the offsets when the batch fits).
+// One workgroup: pair weights, an exclusive scan over requests (weighted
+// offsets), then each slice's first position located by binary search (over
+// an LDS copy of the offsets when the batch fits).
 constexpr int kPlanLdsBatch = 8192;
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
@@ -31,7 +31,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   const int b0 = min(batch, tid * per);
   const int b1 = min(batch, b0 + per);
   int32_t local = 0;
-  for (int b = b0; b < b1; ++b) local += blocks_of(lens[b], mbps);
+  for (int b = b0; b < b1; ++b) local += pair_weight(lens[b], mbps);
   sums[tid] = local;
   __syncthreads();
   for (int off = 1; off < kPlanThreads; off <<= 1) {
@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   for (int b = b0; b < b1; ++b) {
     if (in_lds) sprefix[b] = run * hkv;
     else prefix[b] = run * hkv;
-    run += blocks_of(lens[b], mbps);
+    run += pair_weight(lens[b], mbps);
   }
   const int32_t total = sums[kPlanThreads - 1] * hkv;
   __syncthreads();
@@ -53,30 +53,33 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   const int32_t n = slice_count(total, min_tiles, max_slices, quantum);
   for (int s = tid; s <= n; s += kPlanThreads) {
     SliceStart st;
+    st.pad[0] = st.pad[1] = st.pad[2] = 0;
     if (s == n) {
-      st.tile = total;
+      st.pos = total;
       st.b = batch;
       st.g = 0;
-      st.j = 0;
+      st.x = 0;
+      st.nb = 0;
     } else {
-      const int32_t tile = slice_first_tile(s, total, n);
-      int lo = 0, hi = batch - 1;  // largest b with pre[b] <= tile
+      const int32_t pos = slice_start(s, total, n);
+      int lo = 0, hi = batch - 1;  // largest b with pre[b] <= pos
       while (lo < hi) {
         int mid = (lo + hi + 1) >> 1;
-        if (pre[mid] <= tile) lo = mid; else hi = mid - 1;
+        if (pre[mid] <= pos) lo = mid; else hi = mid - 1;
       }
-      const int32_t nb = blocks_of(lens[lo], mbps);
-      const int32_t r = tile - pre[lo];
-      st.tile = tile;
+      const int32_t w = pair_weight(lens[lo], mbps);
+      const int32_t r = pos - pre[lo];
+      st.pos = pos;
       st.b = lo;
-      st.g = r / nb;
-      st.j = r % nb;
+      st.g = r / w;
+      st.x = r % w;
+      st.nb = w - kPairCost;
     }
     starts[s] = st;
   }
   if (tid == 0) {
     PlanHeader h;
-    h.total_tiles = total;
+    h.total = total;
     h.n_slices = n;
     h.batch = batch;
     h.pad = 0;
@@ -84,26 +87,25 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
 }
 
-// Staged launch: aggregation of the partial outputs of requests cut by slice
-// boundaries (Sec. 4: "aggregate the partial outputs of each request"). Slice
-// w merges the (request, kv head) pair that starts inside it and continues
-// into slice w+1; every contributing slice stored its part normalised, with
-// its log-sum-exp.
+// Staged launch: aggregation of the partial outputs of pairs cut by slice
+// boundaries (Sec. 4: "aggregate the partial outputs of each request"). Wave
+// w looks at boundary s = w + 1: when it falls strictly inside the tiles of a
+// pair whose first tile lies in slice s - 1, that boundary is the first to cut
+// the pair and the wave merges it. Every contributing slice stored its part
+// normalised, with its log-sum-exp.
 template <int G>
 __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = blockIdx.x * kWavesPerGroup + (threadIdx.x >> 6);
-  const int32_t T = p.hdr->total_tiles;
+  const int s = blockIdx.x * kWavesPerGroup + (threadIdx.x >> 6) + 1;
+  const int32_t W = p.hdr->total;
   const int32_t n = p.hdr->n_slices;
-  if (w + 1 >= n) return;
-  const SliceStart s0 = p.starts[w];
-  const SliceStart s1 = p.starts[w + 1];
-  if (s1.j == 0) return;                       // slice w ends on a pair boundary
-  const int32_t pair_first = s1.tile - s1.j;
-  if (pair_first < s0.tile) return;            // an earlier slice owns this pair
-  const int32_t nb = blocks_of(p.lens[s1.b], p.mbps);
-  const int32_t c1 = slice_of_tile(pair_first + nb - 1, T, n);
-  merge_pair<G>(p, s1.b, s1.g, pair_first, w, c1, T, n, lane);
+  if (s >= n) return;
+  const SliceStart a = p.starts[s];
+  if (a.x <= kPairCost) return;                 // no tile of the pair before the boundary
+  const int32_t first_tile = a.pos - a.x + kPairCost;
+  if (first_tile < slice_start(s - 1, W, n)) return;  // an earlier boundary cuts it first
+  const int32_t c1 = slice_of(first_tile + a.nb - 1, W, n);
+  merge_pair<G, false>(p, a.b, a.g, first_tile, s - 1, c1, W, n, lane);
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* __restrict__ dst, size_t words) {

@@ -109,7 +109,7 @@ SMALL_LENS = [1, 15, 16, 17, 31, 33, 100, 257, 1000, 2]
 
 @pytest.mark.parametrize("group", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("variant", ["valu", "mfma"])
-@pytest.mark.parametrize("schedule", ["fused", "staged"])
+@pytest.mark.parametrize("schedule", ["fused", "staged", "two_kernel"])
 def test_small_cases_all_groups(group, variant, schedule):
     hkv = 2
     case = W.build_case(SMALL_LENS, hkv * group, hkv, 128, 16, seed=10 + group)
@@ -222,7 +222,7 @@ def relabel(case, seed):
 
 
 @pytest.mark.parametrize("variant", ["valu", "mfma"])
-@pytest.mark.parametrize("schedule", ["fused", "staged"])
+@pytest.mark.parametrize("schedule", ["fused", "staged", "two_kernel"])
 def test_block_relabeling_is_bit_identical(variant, schedule):
     case = W.make_config(2, 2, batch_limit=24)
     a = run(case, variant=variant, schedule=schedule)
@@ -231,7 +231,7 @@ def test_block_relabeling_is_bit_identical(variant, schedule):
 
 
 @pytest.mark.parametrize("variant", ["valu", "mfma"])
-@pytest.mark.parametrize("schedule", ["fused", "staged"])
+@pytest.mark.parametrize("schedule", ["fused", "staged", "two_kernel"])
 def test_repeated_runs_are_bit_identical(variant, schedule):
     # The fused schedule's arrival counters must be back at zero after each
     # call, or a later call would merge too early or never.
@@ -267,7 +267,7 @@ def test_split_matches_unsplit_and_variants_agree():
     case = W.make_config(5, 105, batch_limit=300)
     base = run(case, variant="mfma", max_slices=1)
     for variant in ("valu", "mfma"):
-        for schedule in ("fused", "staged"):
+        for schedule in ("fused", "staged", "two_kernel"):
             for slices in (0, 64, 1024, neo.MAX_SLICES):
                 y = run(case, variant=variant, schedule=schedule, max_slices=slices)
                 d = float(np.max(np.abs(y - base)))
@@ -282,7 +282,8 @@ def test_schedules_agree_bit_for_bit():
     for variant in ("valu", "mfma"):
         a = run(case, variant=variant, schedule="fused")
         b = run(case, variant=variant, schedule="staged")
-        assert np.array_equal(a, b)
+        c = run(case, variant=variant, schedule="two_kernel")
+        assert np.array_equal(a, b) and np.array_equal(a, c)
 
 
 def test_poisoned_slots_do_not_leak():
@@ -345,6 +346,6 @@ def test_matches_golden_fixture():
     expect = np.array([[[float.fromhex(x) for x in row] for row in head]
                        for head in rec["out_f32_hex"]], dtype=np.float32)
     for variant in ("valu", "mfma"):
-        for schedule in ("staged", "fused"):
+        for schedule in ("staged", "fused", "two_kernel"):
             assert_parity(run(case, variant=variant, schedule=schedule), expect,
                           f"golden {variant} {schedule}")
