@@ -97,10 +97,13 @@ template <int G>
 __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int s = blockIdx.x * kWavesPerGroup + (threadIdx.x >> 6) + 1;
+  if (s > NEO_MAX_SLICES) return;
+  // The header and this boundary's record are loaded together (the record
+  // array always holds NEO_MAX_SLICES + 1 entries; stale ones are not used).
+  const SliceStart a = p.starts[s];
   const int32_t W = p.hdr->total;
   const int32_t n = p.hdr->n_slices;
   if (s >= n) return;
-  const SliceStart a = p.starts[s];
   if (a.x <= kPairCost) return;                 // no tile of the pair before the boundary
   const int32_t first_tile = a.pos - a.x + kPairCost;
   if (first_tile < slice_start(s - 1, W, n)) return;  // an earlier boundary cuts it first
