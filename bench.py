@@ -12,6 +12,7 @@ Cache (each replica holds identical values). Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config N] [--variant auto|valu|mfma]
     python bench.py --copy-calibration     # plain copy of known size, for rocprofv3 --pmc
+    python bench.py --op kv_swap_out|kv_swap_in|kv_copy_d2d|kv_append   # cache operations
 """
 from __future__ import annotations
 
@@ -30,6 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
+PEAK_PCIE_GBS = 64.0           # PCIe 5.0 x16 host link, one direction (32 GT/s x 16 lanes)
 MALL_BYTES = 256 * 2 ** 20     # Infinity Cache
 METRIC = "decode-attention achieved HBM GB/s (% of peak) + tokens/sec per layer, 1 GPU"
 KERNEL_SOURCES = ("decode_mfma.hip", "decode_valu.hip", "decode_common.h", "neo_internal.h")
@@ -136,6 +138,135 @@ def copy_calibration(nbytes: int = 2 ** 30, reps: int = 5):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
 
 
+def bench_kv_op(args, torch, neo, W):
+    """Cache operations on the workload's KV: swap every in-use block out to a
+    pinned host cache (kv_swap_out), back in (kv_swap_in), between two device
+    caches (kv_copy_d2d), or append one token per request (kv_append). Each is
+    one kernel on the current stream; a plain DMA copy of the same byte count
+    (hipMemcpyAsync through torch) is timed beside the swaps for reference."""
+    seed = args.config if args.seed is None else args.seed
+    case = W.make_config(args.config, seed, poison=False)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    used = sorted({int(x) for b, L in enumerate(case.seq_lens.tolist())
+                   for x in case.block_table[b, :(L + 15) // 16]})
+    n = len(used)
+    ids = torch.tensor(used, dtype=torch.int32, device="cuda")
+    seq = torch.arange(n, dtype=torch.int32, device="cuda")
+    blk_bytes = 2 * case.num_kv_heads * 2048 * 2  # K and V of one block, all kv heads
+    hip = HipEvents()
+    sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    dma = None
+    if args.op in ("kv_swap_out", "kv_swap_in", "kv_copy_d2d"):
+        pinned = args.op != "kv_copy_d2d"
+        shape_k, shape_v = (n,) + tuple(k.shape[1:]), (n,) + tuple(v.shape[1:])
+        if pinned:
+            ok_ = torch.empty(shape_k, dtype=torch.bfloat16, pin_memory=True)
+            ov = torch.empty(shape_v, dtype=torch.bfloat16, pin_memory=True)
+        else:
+            ok_ = torch.empty(shape_k, dtype=torch.bfloat16, device="cuda")
+            ov = torch.empty(shape_v, dtype=torch.bfloat16, device="cuda")
+        if args.op == "kv_swap_in":
+            neo.copy_blocks(k, v, ok_, ov, ids, seq)
+            torch.cuda.synchronize()
+
+            def one():
+                neo.copy_blocks(ok_, ov, k, v, seq, ids)
+        else:
+            def one():
+                neo.copy_blocks(k, v, ok_, ov, ids, seq)
+        nbytes = n * blk_bytes
+        bytes_per_call = 2 * nbytes  # read + write
+        link_bytes = nbytes
+        if pinned:
+            dk = k[:n].contiguous() if args.op == "kv_swap_in" else k[:n]
+            dv = v[:n].contiguous() if args.op == "kv_swap_in" else v[:n]
+
+            def dma_one():
+                if args.op == "kv_swap_out":
+                    ok_.copy_(dk, non_blocking=True)
+                    ov.copy_(dv, non_blocking=True)
+                else:
+                    dk.copy_(ok_, non_blocking=True)
+                    dv.copy_(ov, non_blocking=True)
+            dma = dma_one
+    elif args.op == "kv_append":
+        rng = __import__("numpy").random.default_rng(seed)
+        shape = (case.batch, case.num_kv_heads, case.head_dim)
+        kn = torch.from_numpy(rng.integers(0, 1 << 16, size=shape, dtype="uint16").view(
+            "int16")).to("cuda").view(torch.bfloat16)
+        vn = kn.clone()
+
+        def one():
+            neo.kv_append(k, v, kn, vn, bt, sl)
+        nbytes = 2 * kn.numel() * 2
+        bytes_per_call = 2 * nbytes + 4 * case.batch * 2
+        link_bytes = None
+    else:
+        raise SystemExit(f"unknown --op {args.op}")
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = hip.create(), hip.create()
+        hip.record(a, sh)
+        for _ in range(args.steps):
+            fn()
+        hip.record(b, sh)
+        torch.cuda.synchronize()
+        ms = hip.elapsed_ms(a, b) / args.steps
+        hip.destroy(a)
+        hip.destroy(b)
+        return ms
+
+    def per_call(fn):
+        """Mean GPU time of one call from an event pair around each call."""
+        evs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+        for a, b in evs:
+            hip.record(a, sh)
+            fn()
+            hip.record(b, sh)
+        torch.cuda.synchronize()
+        ms = sum(hip.elapsed_ms(a, b) for a, b in evs) / len(evs)
+        for a, b in evs:
+            hip.destroy(a)
+            hip.destroy(b)
+        return ms
+
+    log(f"[bench] {args.op} on {case.name}: {n} blocks in use, {nbytes / 1e6:.1f} MB per call")
+    ms = timed(one)
+    kernel_ms = per_call(one)
+    result = {
+        "metric": f"{args.op} GB/s",
+        "op": args.op,
+        "value": round((link_bytes or bytes_per_call) / (ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "us_per_call": round(ms * 1e3, 3),
+        "kernel_us": round(kernel_ms * 1e3, 3),
+        "bytes_per_call": bytes_per_call,
+        "config": {"workload": f"{case.name}: KV of {case.batch} requests, "
+                               f"{case.num_kv_heads} kv heads, {n} blocks"},
+        "steps": args.steps, "warmup": args.warmup,
+    }
+    if link_bytes is not None:
+        result["roofline"] = {"bound": "pcie", "achieved": result["value"],
+                              "peak": PEAK_PCIE_GBS, "unit": "GB/s",
+                              "frac": round(result["value"] / PEAK_PCIE_GBS, 4)}
+        if args.op == "kv_copy_d2d":
+            hbm = bytes_per_call / (ms * 1e-3) / 1e9
+            result["roofline"] = {"bound": "hbm", "achieved": round(hbm, 2),
+                                  "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                  "frac": round(hbm / PEAK_HBM_GBS, 4)}
+            result["value"] = round(hbm, 2)
+    if dma is not None:
+        dms = timed(dma)
+        result["dma_reference"] = {"what": "hipMemcpyAsync of the same bytes, contiguous",
+                                   "GBs": round(nbytes / (dms * 1e-3) / 1e9, 2),
+                                   "us_per_call": round(dms * 1e3, 3)}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +281,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--op", default="decode",
+                    choices=["decode", "kv_swap_out", "kv_swap_in", "kv_copy_d2d", "kv_append"])
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -164,6 +297,9 @@ def main(argv=None):
 
     import paper_2411_01142_amd as neo
     from paper_2411_01142_amd import workloads as W
+
+    if args.op != "decode":
+        return bench_kv_op(args, torch, neo, W)
 
     seed = args.config if args.seed is None else args.seed
     log(f"[bench] generating config {args.config} seed {seed}")

@@ -169,6 +169,40 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
                             int32_t block_size, int32_t num_blocks, void* dst, void* stream);
 
 /*
+ * Append one token per request (the decoding phase reads and appends the KV
+ * cache, Sec. 2.1). k_new, v_new: device bf16 [batch][num_kv_heads][head_dim],
+ * the key and value rows of each request's newest token; they are written as
+ * token seq_lens[b] - 1 of request b (seq_lens counts the new token): block
+ * block_table[b][(L-1)/block_size], slot (L-1) % block_size, into the K and V
+ * layouts above. Requests with L <= 0 are skipped; lengths past the table are
+ * clamped to it; a block id outside [0, num_blocks) skips the write.
+ * head_dim 128, block_size 16. k_cache and k_new must be 16-byte aligned.
+ */
+neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                         const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                         int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                         int32_t block_size, int32_t num_blocks, void* stream);
+
+/*
+ * Copy whole blocks (all kv heads, K and V) between two caches of the layout
+ * above: for i < n, dst block dst_ids[i] <- src block src_ids[i]. This is the
+ * swap of partial offloading (a request's KV lives wholly in the GPU cache or
+ * wholly in the CPU cache) and of layer-wise swapping (each layer's KV of newly
+ * prefilled requests moves as soon as it is computed), Sec. 3.1. Each cache
+ * pointer may be device memory or pinned host memory the device can address
+ * (hipHostMalloc); any other pointer (pageable host memory) is refused with
+ * NEO_ERR_INVALID_ARG before launch. The copy is one kernel on `stream`, so it
+ * overlaps with attention on another stream. src_ids, dst_ids: int32 [n], same
+ * memory rules; pairs with an id out of range are skipped. Destination blocks
+ * must be distinct and must not be read by the same call (no in-place chains).
+ * head_dim 128, block_size 16; all four caches 16-byte aligned.
+ */
+neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                              const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
+                              int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                              int32_t src_num_blocks, int32_t dst_num_blocks, void* stream);
+
+/*
  * Opt-in check of the indexing inputs: counts seq_lens outside
  * [0, max_blocks_per_seq * block_size] and block-table entries in use
  * (j < ceil(L / block_size)) outside [0, num_blocks). Adds the count to

@@ -57,6 +57,11 @@ def _load():
     lib.neo_ref_lse_merge.restype = ctypes.c_int
     lib.neo_ref_paged_gather.argtypes = [_P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32, _I32, _P]
     lib.neo_ref_paged_gather.restype = ctypes.c_int64
+    lib.neo_ref_kv_append.argtypes = [_P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I32, _I32, _I32]
+    lib.neo_ref_kv_append.restype = _I32
+    lib.neo_ref_copy_blocks.argtypes = [_P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I32, _I32,
+                                        _I32]
+    lib.neo_ref_copy_blocks.restype = _I32
     lib.neo_ref_max_threads.argtypes = []
     lib.neo_ref_max_threads.restype = ctypes.c_int
     _lib = lib
@@ -165,3 +170,28 @@ def paged_gather(case, which: str) -> np.ndarray:
     if n < 0:
         raise OracleError(f"neo_ref_paged_gather failed: {n}")
     return dst[:total]
+
+
+def kv_append(case, k_new: np.ndarray, v_new: np.ndarray) -> int:
+    """Write each request's newest token (k_new, v_new: uint16 [B][Hkv][D]) into the
+    case's caches in place, at token seq_lens[b] - 1. Returns requests written."""
+    lib = _load()
+    assert case.k_cache.flags.c_contiguous and case.v_cache.flags.c_contiguous
+    kn, vn = _c(k_new, np.uint16), _c(v_new, np.uint16)
+    bt, sl = _c(case.block_table, np.int32), _c(case.seq_lens, np.int32)
+    return int(lib.neo_ref_kv_append(_ptr(case.k_cache), _ptr(case.v_cache), _ptr(kn), _ptr(vn),
+                                      _ptr(bt), _ptr(sl), case.batch, case.max_blocks_per_seq,
+                                      case.num_kv_heads, case.head_dim, case.block_size,
+                                      case.num_blocks))
+
+
+def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, num_kv_heads: int,
+                head_dim: int = 128, block_size: int = 16) -> int:
+    """dst block dst_ids[i] <- src block src_ids[i] (uint16 caches, in place)."""
+    lib = _load()
+    assert dst_k.flags.c_contiguous and dst_v.flags.c_contiguous
+    sk, sv = _c(src_k, np.uint16), _c(src_v, np.uint16)
+    si, di = _c(src_ids, np.int32), _c(dst_ids, np.int32)
+    return int(lib.neo_ref_copy_blocks(_ptr(sk), _ptr(sv), _ptr(dst_k), _ptr(dst_v), _ptr(si),
+                                       _ptr(di), int(si.shape[0]), num_kv_heads, head_dim,
+                                       block_size, int(sk.shape[0]), int(dst_k.shape[0])))

@@ -301,3 +301,60 @@ int neo_ref_max_threads(void) {
   return 1;
 #endif
 }
+
+/*
+ * Append (the decoding phase reads and appends the KV cache, Sec. 2.1): the
+ * newest token of request b is token L-1 with L = seq_lens[b] (clamped to the
+ * table); its key and value rows k_new[b][g][:], v_new[b][g][:] go to block
+ * block_table[b][(L-1)/bs], slot (L-1) % bs. L <= 0 or an out-of-range block
+ * id: nothing written. Returns the number of requests written.
+ */
+int32_t neo_ref_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new,
+                          const uint16_t* v_new, const int32_t* block_table,
+                          const int32_t* seq_lens, int32_t batch, int32_t max_blocks_per_seq,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                          int32_t num_blocks) {
+  int32_t written = 0;
+  for (int64_t b = 0; b < batch; ++b) {
+    int64_t L = seq_lens[b];
+    int64_t cap = (int64_t)max_blocks_per_seq * block_size;
+    if (L > cap) L = cap;
+    if (L <= 0) continue;
+    int64_t t = L - 1;
+    int64_t p = block_table[b * max_blocks_per_seq + t / block_size];
+    if (p < 0 || p >= num_blocks) continue;
+    int64_t slot = t % block_size;
+    for (int64_t g = 0; g < num_kv_heads; ++g) {
+      for (int64_t d = 0; d < head_dim; ++d) {
+        int64_t src = (b * num_kv_heads + g) * head_dim + d;
+        k_cache[(((p * num_kv_heads + g) * (head_dim / 8) + d / 8) * block_size + slot) * 8 +
+                d % 8] = k_new[src];
+        v_cache[((p * num_kv_heads + g) * head_dim + d) * block_size + slot] = v_new[src];
+      }
+    }
+    ++written;
+  }
+  return written;
+}
+
+/*
+ * Block copy between two caches of the same layout: dst block dst_ids[i] <-
+ * src block src_ids[i] for every i with both ids in range (all kv heads, K and V).
+ */
+int32_t neo_ref_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
+                            uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
+                            int32_t n, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                            int32_t src_num_blocks, int32_t dst_num_blocks) {
+  int64_t per = (int64_t)num_kv_heads * head_dim * block_size;
+  int32_t copied = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    int64_t s = src_ids[i], d = dst_ids[i];
+    if (s < 0 || s >= src_num_blocks || d < 0 || d >= dst_num_blocks) continue;
+    for (int64_t e = 0; e < per; ++e) {
+      dst_k[d * per + e] = src_k[s * per + e];
+      dst_v[d * per + e] = src_v[s * per + e];
+    }
+    ++copied;
+  }
+  return copied;
+}

@@ -27,7 +27,7 @@ import threading
 __all__ = [
     "NeoError", "decode_attention", "workspace_bytes", "paged_gather", "debug_validate",
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
-    "new_workspace",
+    "new_workspace", "kv_append", "copy_blocks",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -89,6 +89,10 @@ def load_library():
         lib.neo_decode_workspace_init.restype = ctypes.c_int
         lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, P, P]
         lib.neo_paged_gather.restype = ctypes.c_int
+        lib.neo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
+        lib.neo_kv_append.restype = ctypes.c_int
+        lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
+        lib.neo_kv_copy_blocks.restype = ctypes.c_int
         lib.neo_debug_validate.argtypes = [P, P, I, I, I, I, P, P]
         lib.neo_debug_validate.restype = ctypes.c_int
         lib.neo_last_error.argtypes = []
@@ -272,3 +276,62 @@ def debug_validate(block_table, seq_lens, num_blocks: int, block_size: int = 16,
                                       seq_lens.shape[0], block_table.shape[1], int(block_size),
                                       int(num_blocks), cnt.data_ptr(), sh))
     return int(cnt.item())
+
+
+def kv_append(k_cache, v_cache, k_new, v_new, block_table, seq_lens, *, stream=None):
+    """Write each request's newest token (k_new, v_new: bf16 [B, Hkv, 128]) into the
+    paged caches at token seq_lens[b] - 1 (in place, on ``stream``)."""
+    torch = _torch()
+    lib = load_library()
+    _require(k_cache, "k_cache", torch.bfloat16, 5)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    _require(k_new, "k_new", torch.bfloat16, 3)
+    _require(v_new, "v_new", torch.bfloat16, 3)
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(seq_lens, "seq_lens", torch.int32, 1)
+    NB, Hkv, npieces, bs, x = k_cache.shape
+    B = seq_lens.shape[0]
+    if tuple(k_new.shape) != (B, Hkv, npieces * x) or k_new.shape != v_new.shape:
+        raise ValueError("k_new and v_new must be [batch, num_kv_heads, head_dim]")
+    sh = _stream_handle(stream, k_cache.device)
+    with torch.cuda.device(k_cache.device):
+        _check(lib.neo_kv_append(k_cache.data_ptr(), v_cache.data_ptr(), k_new.data_ptr(),
+                                 v_new.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
+                                 B, block_table.shape[1], Hkv, npieces * x, bs, NB, sh))
+
+
+def _cache_arg(t, name, ndim):
+    """A cache tensor on the GPU or in pinned host memory (device-addressable)."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.bfloat16 or t.dim() != ndim:
+        raise TypeError(f"{name} must be a bf16 tensor with {ndim} dims")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device.type != "cuda" and not t.is_pinned():
+        raise ValueError(f"{name} must be on a GPU or in pinned host memory")
+
+
+def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, *, stream=None, device=None):
+    """dst block dst_ids[i] <- src block src_ids[i] for K and V. Caches may be GPU
+    tensors or pinned host tensors (``pin_memory=True``); ids are int32 GPU
+    tensors. Runs as one kernel on ``stream`` (of ``device``, default: the ids')."""
+    torch = _torch()
+    lib = load_library()
+    _cache_arg(src_k, "src_k", 5)
+    _cache_arg(dst_k, "dst_k", 5)
+    _cache_arg(src_v, "src_v", 4)
+    _cache_arg(dst_v, "dst_v", 4)
+    _require(src_ids, "src_ids", torch.int32, 1)
+    _require(dst_ids, "dst_ids", torch.int32, 1)
+    if src_ids.shape != dst_ids.shape:
+        raise ValueError("src_ids and dst_ids must have the same length")
+    if src_k.shape[1:] != dst_k.shape[1:] or src_v.shape[1:] != dst_v.shape[1:]:
+        raise ValueError("source and destination caches must share the block layout")
+    NB_s, Hkv, npieces, bs, x = src_k.shape
+    device = src_ids.device if device is None else device
+    sh = _stream_handle(stream, device)
+    with torch.cuda.device(device):
+        _check(lib.neo_kv_copy_blocks(src_k.data_ptr(), src_v.data_ptr(), dst_k.data_ptr(),
+                                      dst_v.data_ptr(), src_ids.data_ptr(), dst_ids.data_ptr(),
+                                      src_ids.shape[0], Hkv, npieces * x, bs, NB_s,
+                                      dst_k.shape[0], sh))

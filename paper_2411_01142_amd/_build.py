@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libneoattn.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["api.hip", "plan_combine.hip", "decode_mfma.hip", "decode_valu.hip"]
+SOURCES = ["api.hip", "plan_combine.hip", "decode_mfma.hip", "decode_valu.hip", "kv_ops.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall",

@@ -32,6 +32,32 @@ neo_status ok() {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+// Address the device uses for `p`: `p` itself for device or managed memory,
+// the mapped device address for pinned host memory, NULL for anything else
+// (pageable host memory, unknown pointers). Clears the error HIP records for
+// an unknown pointer.
+void* device_address(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  switch (a.type) {
+    case hipMemoryTypeDevice:
+    case hipMemoryTypeManaged:
+      return const_cast<void*>(p);
+    case hipMemoryTypeHost:
+      // The mapped address of `p` itself, whether the runtime reports the
+      // allocation's base or `p` (the offset from hostPointer is kept).
+      if (!a.devicePointer) return nullptr;
+      return static_cast<char*>(a.devicePointer) +
+             (a.hostPointer ? static_cast<const char*>(p) - static_cast<const char*>(a.hostPointer)
+                            : 0);
+    default:
+      return nullptr;
+  }
+}
+
 bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
 
 // Compute units of the current device, cached per device ordinal. The default
@@ -265,6 +291,70 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
                                     num_kv_heads, head_dim, block_size, num_blocks,
                                     static_cast<uint16_t*>(dst), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(NEO_ERR_HIP, "gather launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                         const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                         int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                         int32_t block_size, int32_t num_blocks, void* stream) {
+  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (num_kv_heads <= 0) return fail(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
+  if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
+    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
+                head_dim, block_size);
+  if (batch == 0) return ok();
+  if (!k_cache || !v_cache || !k_new || !v_new || !block_table || !seq_lens)
+    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  if (!aligned(k_cache, 16) || !aligned(k_new, 16) || !aligned(v_cache, 2) || !aligned(v_new, 2))
+    return fail(NEO_ERR_INVALID_ARG, "k_cache and k_new must be 16-byte aligned");
+  hipError_t e = neo::launch_kv_append(
+      static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
+      static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), block_table,
+      seq_lens, batch, max_blocks_per_seq, num_kv_heads, num_blocks,
+      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "append launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                              const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
+                              int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                              int32_t src_num_blocks, int32_t dst_num_blocks, void* stream) {
+  if (n < 0) return fail(NEO_ERR_INVALID_ARG, "n (%d) is negative", n);
+  if (num_kv_heads <= 0) return fail(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
+  if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
+    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
+                head_dim, block_size);
+  if (n == 0) return ok();
+  if (!src_k || !src_v || !dst_k || !dst_v || !src_ids || !dst_ids)
+    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (src_num_blocks <= 0 || dst_num_blocks <= 0)
+    return fail(NEO_ERR_INVALID_ARG, "block counts must be positive");
+  if (!aligned(src_k, 16) || !aligned(src_v, 16) || !aligned(dst_k, 16) || !aligned(dst_v, 16))
+    return fail(NEO_ERR_INVALID_ARG, "caches must be 16-byte aligned");
+  // Every pointer the kernel dereferences must be device memory or pinned host
+  // memory; pageable host memory would fault the kernel, so it is refused here.
+  const void* ptrs[6] = {src_k, src_v, dst_k, dst_v, src_ids, dst_ids};
+  void* dev[6];
+  static const char* names[6] = {"src_k", "src_v", "dst_k", "dst_v", "src_ids", "dst_ids"};
+  for (int i = 0; i < 6; ++i) {
+    dev[i] = device_address(ptrs[i]);
+    if (!dev[i])
+      return fail(NEO_ERR_INVALID_ARG,
+                  "%s is not device memory or pinned host memory the device can address",
+                  names[i]);
+  }
+  hipError_t e = neo::launch_copy_blocks(
+      static_cast<const uint16_t*>(dev[0]), static_cast<const uint16_t*>(dev[1]),
+      static_cast<uint16_t*>(dev[2]), static_cast<uint16_t*>(dev[3]),
+      static_cast<const int32_t*>(dev[4]), static_cast<const int32_t*>(dev[5]), n, num_kv_heads,
+      src_num_blocks, dst_num_blocks, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(NEO_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -1,0 +1,109 @@
+// The two cache operations on either side of decode attention:
+//
+//  * append: the decoding phase reads and appends the KV cache (Sec. 2.1);
+//    the new token's key and value rows are written into their paged slot;
+//  * block copy: whole (block, all kv heads) runs of K and V moved between two
+//    caches, e.g. the GPU cache in HBM and a CPU cache in pinned host memory
+//    (partial offloading and layer-wise swapping, Sec. 3.1). The copy is a
+//    kernel on the caller's stream, so it overlaps with attention running on
+//    another stream, and pinned host memory is read or written directly over
+//    the host link in 16-byte accesses.
+#include "neo_internal.h"
+
+namespace neo {
+namespace {
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// One workgroup per request: thread items are (kv head, 16-byte key piece)
+// for K and (kv head, dim) for V.
+__global__ __launch_bounds__(256) void append_kernel(
+    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
+    const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
+    const int32_t* __restrict__ table, const int32_t* __restrict__ lens, int32_t mbps,
+    int32_t hkv, int32_t num_blocks) {
+  const int b = blockIdx.x;
+  const int32_t L = clamp_len(lens[b], mbps);
+  if (L <= 0) return;
+  const int32_t t = L - 1;
+  const int32_t blk = table[(size_t)b * mbps + t / kBlock];
+  if (blk < 0 || blk >= num_blocks) return;
+  const int slot = t % kBlock;
+  const size_t tile0 = (size_t)blk * hkv * kTileElems;
+  const int pieces = kHeadDim / kPiece;
+  for (int it = threadIdx.x; it < hkv * pieces; it += blockDim.x) {
+    const int g = it / pieces, c = it % pieces;
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(
+        k_new + ((size_t)b * hkv + g) * kHeadDim + c * kPiece);
+    *reinterpret_cast<u32x4_t*>(k_cache + tile0 + (size_t)g * kTileElems +
+                                ((size_t)c * kBlock + slot) * kPiece) = v;
+  }
+  for (int it = threadIdx.x; it < hkv * kHeadDim; it += blockDim.x) {
+    const int g = it / kHeadDim, d = it % kHeadDim;
+    v_cache[tile0 + (size_t)g * kTileElems + (size_t)d * kBlock + slot] =
+        v_new[((size_t)b * hkv + g) * kHeadDim + d];
+  }
+}
+
+// One workgroup per copied block: K and V, 16 bytes per access, four words of
+// each cache loaded before any is stored so that reads over the host link
+// keep eight requests in flight per thread.
+__global__ __launch_bounds__(256) void copy_blocks_kernel(
+    const uint16_t* __restrict__ src_k, const uint16_t* __restrict__ src_v,
+    uint16_t* __restrict__ dst_k, uint16_t* __restrict__ dst_v,
+    const int32_t* __restrict__ src_ids, const int32_t* __restrict__ dst_ids, int32_t hkv,
+    int32_t src_blocks, int32_t dst_blocks) {
+  constexpr int kUnroll = 4;
+  const int i = blockIdx.x;
+  const int32_t s = src_ids[i], d = dst_ids[i];
+  if (s < 0 || s >= src_blocks || d < 0 || d >= dst_blocks) return;
+  // 16-byte words per block per cache: hkv * 256, a multiple of blockDim.
+  const int words = hkv * (kTileElems / 8);
+  const u32x4_t* sk = reinterpret_cast<const u32x4_t*>(src_k) + (size_t)s * words;
+  const u32x4_t* sv = reinterpret_cast<const u32x4_t*>(src_v) + (size_t)s * words;
+  u32x4_t* dk = reinterpret_cast<u32x4_t*>(dst_k) + (size_t)d * words;
+  u32x4_t* dv = reinterpret_cast<u32x4_t*>(dst_v) + (size_t)d * words;
+  for (int w0 = 0; w0 < words; w0 += kUnroll * 256) {
+    // Rows of 256 words left in this step (fewer than kUnroll only at the end).
+    const int rows = min(kUnroll, (words - w0) / 256);
+    u32x4_t a[kUnroll], c[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (u < rows) {
+        const int w = w0 + u * 256 + threadIdx.x;
+        a[u] = sk[w];
+        c[u] = sv[w];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (u < rows) {
+        const int w = w0 + u * 256 + threadIdx.x;
+        dk[w] = a[u];
+        dv[w] = c[u];
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new,
+                            const uint16_t* v_new, const int32_t* table, const int32_t* lens,
+                            int32_t batch, int32_t mbps, int32_t hkv, int32_t num_blocks,
+                            hipStream_t stream) {
+  append_kernel<<<batch, 256, 0, stream>>>(k_cache, v_cache, k_new, v_new, table, lens, mbps, hkv,
+                                           num_blocks);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
+                              uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
+                              int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
+                              hipStream_t stream) {
+  copy_blocks_kernel<<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, hkv,
+                                            src_blocks, dst_blocks);
+  return hipGetLastError();
+}
+
+}  // namespace neo

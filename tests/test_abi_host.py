@@ -34,7 +34,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("neo_decode_attention", "neo_decode_attention_ex", "neo_decode_workspace_bytes",
               "neo_decode_workspace_init", "neo_decode_attention_events",
-              "neo_paged_gather", "neo_debug_validate", "neo_last_error", "neo_version"):
+              "neo_paged_gather", "neo_kv_append", "neo_kv_copy_blocks", "neo_debug_validate",
+              "neo_last_error", "neo_version"):
         assert n in names
 
 
@@ -107,7 +108,7 @@ def call(lib, **kw):
     (dict(out=FAKE + 4), INVALID, "aligned"),
     (dict(ws=FAKE + 64), INVALID, "aligned"),
     (dict(variant=7), UNSUPPORTED, "variant"),
-    (dict(schedule=3), UNSUPPORTED, "schedule"),
+    (dict(schedule=4), UNSUPPORTED, "schedule"),
     (dict(slices=-1), INVALID, "max_slices"),
     (dict(slices=100000), INVALID, "max_slices"),
     (dict(batch=1 << 20, mbps=1 << 12), INVALID, "2^31"),
@@ -142,6 +143,54 @@ def test_gather_and_validate_reject(lib):
     assert lib.neo_debug_validate(None, FAKE, 4, 8, 16, 100, FAKE, None) == INVALID
     assert lib.neo_decode_workspace_init(None, 1024, None) == INVALID
     assert lib.neo_decode_workspace_init(FAKE + 4, 1024, None) == INVALID
+
+
+def append_call(lib, **kw):
+    a = dict(k=FAKE, v=FAKE, kn=FAKE, vn=FAKE, table=FAKE, lens=FAKE, batch=4, mbps=8, hkv=8,
+             d=128, bs=16, nb=100)
+    a.update(kw)
+    return lib.neo_kv_append(a["k"], a["v"], a["kn"], a["vn"], a["table"], a["lens"], a["batch"],
+                             a["mbps"], a["hkv"], a["d"], a["bs"], a["nb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=-1), INVALID), (dict(hkv=0), INVALID), (dict(d=64), UNSUPPORTED),
+    (dict(bs=8), UNSUPPORTED), (dict(k=None), INVALID), (dict(vn=None), INVALID),
+    (dict(table=None), INVALID), (dict(mbps=0), INVALID), (dict(nb=0), INVALID),
+    (dict(k=FAKE + 2), INVALID), (dict(kn=FAKE + 8), INVALID), (dict(v=FAKE + 1), INVALID),
+    (dict(mbps=1 << 28), INVALID),
+])
+def test_kv_append_rejects(lib, kw, code):
+    assert append_call(lib, **kw) == code
+    assert lib.neo_last_error().decode()
+
+
+def test_kv_append_empty_batch_is_a_noop(lib):
+    assert append_call(lib, batch=0, k=None, v=None, kn=None, vn=None, table=None,
+                       lens=None) == OK
+
+
+def copy_call(lib, **kw):
+    a = dict(sk=FAKE, sv=FAKE, dk=FAKE, dv=FAKE, si=FAKE, di=FAKE, n=4, hkv=8, d=128, bs=16,
+             snb=100, dnb=100)
+    a.update(kw)
+    return lib.neo_kv_copy_blocks(a["sk"], a["sv"], a["dk"], a["dv"], a["si"], a["di"], a["n"],
+                                  a["hkv"], a["d"], a["bs"], a["snb"], a["dnb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=-1), INVALID), (dict(hkv=-2), INVALID), (dict(d=256), UNSUPPORTED),
+    (dict(bs=32), UNSUPPORTED), (dict(sk=None), INVALID), (dict(dv=None), INVALID),
+    (dict(di=None), INVALID), (dict(snb=0), INVALID), (dict(dnb=-5), INVALID),
+    (dict(sv=FAKE + 8), INVALID), (dict(dk=FAKE + 4), INVALID),
+])
+def test_kv_copy_blocks_rejects(lib, kw, code):
+    assert copy_call(lib, **kw) == code
+    assert lib.neo_last_error().decode()
+
+
+def test_kv_copy_blocks_zero_blocks_is_a_noop(lib):
+    assert copy_call(lib, n=0, sk=None, sv=None, dk=None, dv=None, si=None, di=None) == OK
 
 
 def test_python_binding_refuses_cpu_tensors():
