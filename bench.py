@@ -13,6 +13,7 @@ Cache (each replica holds identical values). Prints one JSON line.
     python bench.py [--steps K] [--warmup W] [--config N] [--variant auto|valu|mfma]
     python bench.py --copy-calibration     # plain copy of known size, for rocprofv3 --pmc
     python bench.py --op kv_swap_out|kv_swap_in|kv_copy_d2d|kv_append   # cache operations
+    python bench.py --op cpu_decode [--cpu-threads N] [--cpu-isa ...]   # host-CPU attention
 """
 from __future__ import annotations
 
@@ -267,6 +268,73 @@ def bench_kv_op(args, torch, neo, W):
     return 0
 
 
+def bench_cpu_decode(args, neo, W):
+    """Decode attention on the host CPU over the workload's KV in host memory,
+    against the host's measured read ceiling (the library's read probe over a
+    buffer twice the cache size, same thread count)."""
+    import numpy as np
+    seed = args.config if args.seed is None else args.seed
+    case = W.make_config(args.config, seed, poison=False)
+    threads = args.cpu_threads or neo.cpu_default_threads()
+    isa = neo.cpu_best_isa() if args.cpu_isa == "auto" else args.cpu_isa
+    out = np.empty((case.batch, case.num_q_heads, case.head_dim), np.float32)
+
+    def one():
+        neo.cpu_decode_attention(case.q, case.k_cache, case.v_cache, case.block_table,
+                                 case.seq_lens, case.scale, out, num_threads=threads, isa=isa)
+    log(f"[bench] cpu_decode {case.name}: {threads} threads, isa {isa}")
+    for _ in range(max(1, args.warmup)):
+        one()
+    times = []
+    for _ in range(args.steps):
+        t0 = time.perf_counter()
+        one()
+        times.append(time.perf_counter() - t0)
+    times.sort()
+    med = times[len(times) // 2]
+    alg = case.algorithmic_bytes()
+    gbs = alg / med / 1e9
+    probe = np.ones(max(2 * (case.k_cache.nbytes + case.v_cache.nbytes), 1 << 30) // 4,
+                    np.float32)
+    neo.cpu_read_probe(probe, threads)
+    pt = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        neo.cpu_read_probe(probe, threads)
+        pt.append(time.perf_counter() - t0)
+    ceiling = probe.nbytes / sorted(pt)[2] / 1e9
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    result = {
+        "metric": "cpu decode-attention achieved host-memory GB/s",
+        "op": "cpu_decode",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "ms_per_call": round(med * 1e3, 3),
+        "p10_ms": round(times[len(times) // 10] * 1e3, 3),
+        "p90_ms": round(times[(len(times) * 9) // 10] * 1e3, 3),
+        "tokens_per_s_per_layer": round(case.batch / med, 1),
+        "steps": args.steps, "warmup": args.warmup,
+        "dtype": "bf16", "accumulate": "fp32",
+        "config": {"workload": f"{case.name}: decode attention on the host CPU, "
+                               f"{case.num_q_heads}/{case.num_kv_heads} heads, batch "
+                               f"{case.batch}, seq_lens {SEQ_DESC[args.config]}",
+                   "threads": threads, "isa": isa, "cpu": cpu_model},
+        "roofline": {"bound": "host-dram", "achieved": round(gbs, 2),
+                     "peak": round(ceiling, 2), "unit": "GB/s",
+                     "frac": round(gbs / ceiling, 4),
+                     "peak_kind": "measured read ceiling (library read probe, same threads)"},
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,13 +350,22 @@ def main(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--op", default="decode",
-                    choices=["decode", "kv_swap_out", "kv_swap_in", "kv_copy_d2d", "kv_append"])
+                    choices=["decode", "kv_swap_out", "kv_swap_in", "kv_copy_d2d", "kv_append",
+                             "cpu_decode"])
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--cpu-isa", default="auto",
+                    choices=["auto", "generic", "avx512", "avx512_bf16"])
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the decode-attention path needs no "
               "collective and this build runs on a single MI355X (--gpus 1).", file=sys.stderr)
         return 2
+
+    if args.op == "cpu_decode":
+        import paper_2411_01142_amd as neo
+        from paper_2411_01142_amd import workloads as W
+        return bench_cpu_decode(args, neo, W)
 
     import torch
     if args.copy_calibration:

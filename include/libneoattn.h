@@ -203,6 +203,61 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
                               int32_t src_num_blocks, int32_t dst_num_blocks, void* stream);
 
 /*
+ * Decode attention on the host CPU over a KV cache in host memory (the CPU
+ * half of offloaded decoding, Sec. 4: PACPU). Same arguments, layouts, result
+ * and clamping rules as neo_decode_attention, but every pointer is host
+ * memory (pageable or pinned) and the call is synchronous: it returns when
+ * `out` is written. Work is split at block granularity into equal shares for
+ * `num_threads` threads (0: NEO_CPU_THREADS, else OMP_NUM_THREADS, else the
+ * CPUs this process may run on); the partial outputs of a request split
+ * between threads are aggregated by their log-sum-exps. Block ids in use are
+ * checked against [0, num_blocks) before any is read (NEO_ERR_INVALID_ARG).
+ * The library keeps one pool of worker threads and a host scratch buffer for
+ * the process; concurrent calls are serialised.
+ */
+neo_status neo_cpu_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                                    const int32_t* block_table, const int32_t* seq_lens,
+                                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                    int32_t block_size, float scale, float* out, int32_t batch,
+                                    int32_t max_blocks_per_seq, int32_t num_blocks,
+                                    int32_t num_threads);
+
+/* Instruction-set paths of the CPU attention. */
+typedef enum {
+  NEO_CPU_ISA_AUTO = 0,        /* the best this CPU supports */
+  NEO_CPU_ISA_GENERIC = 1,     /* portable scalar code */
+  NEO_CPU_ISA_AVX512_BF16 = 2, /* AVX-512 with BF16 dot products (vdpbf16ps) */
+  NEO_CPU_ISA_AVX512 = 3       /* AVX-512F, bf16 widened to fp32, fp32 FMAs */
+} neo_cpu_isa;
+
+/* neo_cpu_decode_attention with an explicit path; a path this CPU lacks is
+ * NEO_ERR_UNSUPPORTED. */
+neo_status neo_cpu_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* block_table, const int32_t* seq_lens,
+                                       int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t head_dim, int32_t block_size, float scale,
+                                       float* out, int32_t batch, int32_t max_blocks_per_seq,
+                                       int32_t num_blocks, int32_t num_threads, int32_t isa);
+
+/* The path NEO_CPU_ISA_AUTO takes on this CPU: the environment variable
+ * NEO_CPU_ISA (generic, avx512, avx512_bf16) when this CPU has it, else
+ * AVX512 on any AVX-512 CPU, else GENERIC. */
+int32_t neo_cpu_best_isa(void);
+
+/* Threads a call with num_threads = 0 uses. */
+int32_t neo_cpu_default_threads(void);
+
+/*
+ * Host memory read probe: `num_threads` threads (0: as above) of the CPU
+ * attention's pool each sum one contiguous share of `bytes` (a multiple of
+ * 64) at `buf`, with the widest loads this CPU has; *checksum receives the
+ * sum. Timing a call gives the read bandwidth the CPU attention competes
+ * for (its roofline, and the CPU-side input of a cost model).
+ */
+neo_status neo_cpu_read_probe(const void* buf, size_t bytes, int32_t num_threads,
+                              double* checksum);
+
+/*
  * Opt-in check of the indexing inputs: counts seq_lens outside
  * [0, max_blocks_per_seq * block_size] and block-table entries in use
  * (j < ceil(L / block_size)) outside [0, num_blocks). Adds the count to

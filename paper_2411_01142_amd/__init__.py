@@ -27,12 +27,14 @@ import threading
 __all__ = [
     "NeoError", "decode_attention", "workspace_bytes", "paged_gather", "debug_validate",
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
-    "new_workspace", "kv_append", "copy_blocks",
+    "new_workspace", "kv_append", "copy_blocks", "cpu_decode_attention", "CPU_ISAS",
+    "cpu_best_isa", "cpu_default_threads", "cpu_read_probe",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libneoattn.so")
 
+CPU_ISAS = {"auto": 0, "generic": 1, "avx512_bf16": 2, "avx512": 3}
 VARIANTS = {"auto": 0, "valu": 1, "mfma": 2}
 SCHEDULES = {"auto": 0, "fused": 1, "staged": 2, "two_kernel": 3}
 MAX_SLICES = 4096
@@ -93,6 +95,16 @@ def load_library():
         lib.neo_kv_append.restype = ctypes.c_int
         lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
         lib.neo_kv_copy_blocks.restype = ctypes.c_int
+        lib.neo_cpu_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I, I]
+        lib.neo_cpu_decode_attention_ex.restype = ctypes.c_int
+        lib.neo_cpu_decode_attention.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I]
+        lib.neo_cpu_decode_attention.restype = ctypes.c_int
+        lib.neo_cpu_read_probe.argtypes = [P, ctypes.c_size_t, I, ctypes.POINTER(ctypes.c_double)]
+        lib.neo_cpu_read_probe.restype = ctypes.c_int
+        lib.neo_cpu_best_isa.argtypes = []
+        lib.neo_cpu_best_isa.restype = ctypes.c_int32
+        lib.neo_cpu_default_threads.argtypes = []
+        lib.neo_cpu_default_threads.restype = ctypes.c_int32
         lib.neo_debug_validate.argtypes = [P, P, I, I, I, I, P, P]
         lib.neo_debug_validate.restype = ctypes.c_int
         lib.neo_last_error.argtypes = []
@@ -335,3 +347,71 @@ def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, *, stream=None, de
                                       dst_v.data_ptr(), src_ids.data_ptr(), dst_ids.data_ptr(),
                                       src_ids.shape[0], Hkv, npieces * x, bs, NB_s,
                                       dst_k.shape[0], sh))
+
+
+def cpu_best_isa() -> str:
+    """The CPU attention path ``isa="auto"`` takes on this host."""
+    code = load_library().neo_cpu_best_isa()
+    return {v: k for k, v in CPU_ISAS.items()}[code]
+
+
+def cpu_default_threads() -> int:
+    return int(load_library().neo_cpu_default_threads())
+
+
+def _host_array(a, name, dtype_np, ndim):
+    """(pointer, keep-alive) of a C-contiguous host array: numpy of ``dtype_np``
+    or a CPU torch tensor of the matching dtype (bf16 for uint16 storage)."""
+    import numpy as np
+    try:
+        torch = _torch()
+    except ImportError:  # pragma: no cover
+        torch = None
+    if torch is not None and isinstance(a, torch.Tensor):
+        if a.device.type != "cpu":
+            raise ValueError(f"{name} must be in host memory (got {a.device})")
+        want = {np.uint16: torch.bfloat16, np.int32: torch.int32, np.float32: torch.float32}
+        if a.dtype != want[dtype_np] or a.dim() != ndim or not a.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {want[dtype_np]} tensor with {ndim} dims")
+        return a.data_ptr(), a
+    if not isinstance(a, np.ndarray) or a.dtype != dtype_np or a.ndim != ndim or \
+            not a.flags.c_contiguous:
+        raise ValueError(f"{name} must be a C-contiguous {np.dtype(dtype_np)} array with {ndim} dims")
+    return a.ctypes.data, a
+
+
+def cpu_decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out=None, *,
+                         num_threads: int = 0, isa: str = "auto"):
+    """Decode attention on the host CPU over host-memory caches (same layouts as
+    ``decode_attention``). bf16 data is passed as numpy uint16 arrays (bit
+    patterns) or CPU bf16 tensors. Returns ``out``: float32 [B, Hq, 128]."""
+    import numpy as np
+    lib = load_library()
+    qp, _ = _host_array(q, "q", np.uint16, 3)
+    kp, _ = _host_array(k_cache, "k_cache", np.uint16, 5)
+    vp, _ = _host_array(v_cache, "v_cache", np.uint16, 4)
+    bp, _ = _host_array(block_table, "block_table", np.int32, 2)
+    lp, _ = _host_array(seq_lens, "seq_lens", np.int32, 1)
+    B, Hq, D = q.shape
+    NB, Hkv, npieces, bs, x = k_cache.shape
+    if out is None:
+        out = np.empty((B, Hq, D), dtype=np.float32)
+    op, _ = _host_array(out, "out", np.float32, 3)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    _check(lib.neo_cpu_decode_attention_ex(qp, kp, vp, bp, lp, Hq, Hkv, D, bs, float(scale), op,
+                                           B, block_table.shape[1], NB, int(num_threads),
+                                           CPU_ISAS[isa]))
+    return out
+
+
+def cpu_read_probe(buf, num_threads: int = 0) -> float:
+    """Read the whole host array ``buf`` (size a multiple of 64 bytes) once with the
+    CPU attention's thread pool; returns the checksum (time the call for GB/s)."""
+    import numpy as np
+    if not isinstance(buf, np.ndarray) or not buf.flags.c_contiguous:
+        raise ValueError("buf must be a C-contiguous numpy array")
+    out = ctypes.c_double(0.0)
+    _check(load_library().neo_cpu_read_probe(buf.ctypes.data, buf.nbytes, int(num_threads),
+                                             ctypes.byref(out)))
+    return out.value

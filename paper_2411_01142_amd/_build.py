@@ -15,6 +15,11 @@ LIB = os.path.join(PKG, "libneoattn.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["api.hip", "plan_combine.hip", "decode_mfma.hip", "decode_valu.hip", "kv_ops.hip"]
+# Host-only C++ (the CPU attention), built with the host compiler; its
+# ISA-specific functions carry target attributes and are picked at run time.
+HOST_SOURCES = ["cpu_attention.cpp"]
+HOST_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-pthread", "-fno-math-errno",
+              "-I" + INCLUDE, "-I" + CSRC]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall",
@@ -31,9 +36,19 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; libneoattn needs ROCm's hipcc to build")
 
 
+def cxx() -> str:
+    for cand in (os.environ.get("CXX"), shutil.which("g++"), shutil.which("c++")):
+        if cand:
+            return cand
+    raise RuntimeError("no host C++ compiler (g++) found")
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    if src in HOST_SOURCES:
+        cmd = [cxx(), *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    else:
+        cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{res.stdout}\n{res.stderr}")
@@ -43,10 +58,11 @@ def _compile(src: str) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source and link libneoattn.so (always rebuilds)."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+    srcs = SOURCES + HOST_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = list(ex.map(_compile, srcs))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")

@@ -9,13 +9,16 @@
 #include <atomic>
 #include <string>
 
+#include "neo_error.h"
 #include "neo_internal.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
 
-neo_status fail(neo_status st, const char* fmt, ...) {
+namespace neo {
+
+neo_status set_error(neo_status st, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -25,10 +28,21 @@ neo_status fail(neo_status st, const char* fmt, ...) {
   return st;
 }
 
-neo_status ok() {
+neo_status clear_error() {
   g_last_error.clear();
   return NEO_OK;
 }
+
+}  // namespace neo
+
+namespace {
+
+template <typename... A>
+neo_status fail(neo_status st, const char* fmt, A... a) {
+  return neo::set_error(st, fmt, a...);
+}
+
+neo_status ok() { return neo::clear_error(); }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
@@ -310,6 +324,8 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
     return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
     return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  if ((int64_t)batch * num_kv_heads >= ((int64_t)1 << 31))
+    return fail(NEO_ERR_INVALID_ARG, "batch * num_kv_heads must be below 2^31");
   if (!aligned(k_cache, 16) || !aligned(k_new, 16) || !aligned(v_cache, 2) || !aligned(v_new, 2))
     return fail(NEO_ERR_INVALID_ARG, "k_cache and k_new must be 16-byte aligned");
   hipError_t e = neo::launch_kv_append(

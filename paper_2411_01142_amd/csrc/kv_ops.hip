@@ -15,34 +15,29 @@ namespace {
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-// One workgroup per request: thread items are (kv head, 16-byte key piece)
-// for K and (kv head, dim) for V.
-__global__ __launch_bounds__(256) void append_kernel(
+// One workgroup of 128 threads per (request, kv head): thread d writes dim d
+// of the value row (a 2-byte store: V is dim-major, so the token's dims are
+// 32 bytes apart), threads 0-15 also write one 16-byte key piece each.
+__global__ __launch_bounds__(128) void append_kernel(
     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
     const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
     const int32_t* __restrict__ table, const int32_t* __restrict__ lens, int32_t mbps,
     int32_t hkv, int32_t num_blocks) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x / hkv, g = blockIdx.x % hkv;
   const int32_t L = clamp_len(lens[b], mbps);
   if (L <= 0) return;
   const int32_t t = L - 1;
   const int32_t blk = table[(size_t)b * mbps + t / kBlock];
   if (blk < 0 || blk >= num_blocks) return;
   const int slot = t % kBlock;
-  const size_t tile0 = (size_t)blk * hkv * kTileElems;
-  const int pieces = kHeadDim / kPiece;
-  for (int it = threadIdx.x; it < hkv * pieces; it += blockDim.x) {
-    const int g = it / pieces, c = it % pieces;
-    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(
-        k_new + ((size_t)b * hkv + g) * kHeadDim + c * kPiece);
-    *reinterpret_cast<u32x4_t*>(k_cache + tile0 + (size_t)g * kTileElems +
-                                ((size_t)c * kBlock + slot) * kPiece) = v;
+  const size_t tile = ((size_t)blk * hkv + g) * kTileElems;
+  const size_t src = ((size_t)b * hkv + g) * kHeadDim;
+  const int d = threadIdx.x;
+  if (d < kHeadDim / kPiece) {
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(k_new + src + d * kPiece);
+    *reinterpret_cast<u32x4_t*>(k_cache + tile + ((size_t)d * kBlock + slot) * kPiece) = v;
   }
-  for (int it = threadIdx.x; it < hkv * kHeadDim; it += blockDim.x) {
-    const int g = it / kHeadDim, d = it % kHeadDim;
-    v_cache[tile0 + (size_t)g * kTileElems + (size_t)d * kBlock + slot] =
-        v_new[((size_t)b * hkv + g) * kHeadDim + d];
-  }
+  v_cache[tile + (size_t)d * kBlock + slot] = v_new[src + d];
 }
 
 // One workgroup per copied block: K and V, 16 bytes per access, four words of
@@ -92,8 +87,8 @@ hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t
                             const uint16_t* v_new, const int32_t* table, const int32_t* lens,
                             int32_t batch, int32_t mbps, int32_t hkv, int32_t num_blocks,
                             hipStream_t stream) {
-  append_kernel<<<batch, 256, 0, stream>>>(k_cache, v_cache, k_new, v_new, table, lens, mbps, hkv,
-                                           num_blocks);
+  append_kernel<<<(unsigned)batch * hkv, kHeadDim, 0, stream>>>(k_cache, v_cache, k_new, v_new,
+                                                               table, lens, mbps, hkv, num_blocks);
   return hipGetLastError();
 }
 

@@ -158,7 +158,7 @@ def append_call(lib, **kw):
     (dict(bs=8), UNSUPPORTED), (dict(k=None), INVALID), (dict(vn=None), INVALID),
     (dict(table=None), INVALID), (dict(mbps=0), INVALID), (dict(nb=0), INVALID),
     (dict(k=FAKE + 2), INVALID), (dict(kn=FAKE + 8), INVALID), (dict(v=FAKE + 1), INVALID),
-    (dict(mbps=1 << 28), INVALID),
+    (dict(mbps=1 << 28), INVALID), (dict(batch=1 << 28, hkv=16), INVALID),
 ])
 def test_kv_append_rejects(lib, kw, code):
     assert append_call(lib, **kw) == code
