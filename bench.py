@@ -359,7 +359,7 @@ def main(argv=None):
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the decode-attention path needs no "
-              "collective and this build runs on a single MI355X (--gpus 1).", file=sys.stderr)
+              "collective, and the benchmark runs on a single MI355X (--gpus 1).", file=sys.stderr)
         return 2
 
     if args.op == "cpu_decode":

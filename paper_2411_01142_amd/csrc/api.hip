@@ -10,6 +10,7 @@
 #include <string>
 
 #include "neo_error.h"
+#include "kv_ops.h"
 #include "neo_internal.h"
 
 namespace {

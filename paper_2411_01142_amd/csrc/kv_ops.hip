@@ -8,6 +8,7 @@
 //    kernel on the caller's stream, so it overlaps with attention running on
 //    another stream, and pinned host memory is read or written directly over
 //    the host link in 16-byte accesses.
+#include "kv_ops.h"
 #include "neo_internal.h"
 
 namespace neo {

@@ -119,14 +119,6 @@ hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* tab
                          const int32_t* lens, const int32_t* offsets, int32_t batch,
                          int32_t mbps, int32_t hkv, int32_t head_dim, int32_t block_size,
                          int32_t num_blocks, uint16_t* dst, hipStream_t stream);
-hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new,
-                            const uint16_t* v_new, const int32_t* table, const int32_t* lens,
-                            int32_t batch, int32_t mbps, int32_t hkv, int32_t num_blocks,
-                            hipStream_t stream);
-hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
-                              uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
-                              int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
-                              hipStream_t stream);
 hipError_t launch_validate(const int32_t* table, const int32_t* lens, int32_t batch,
                            int32_t mbps, int32_t block_size, int32_t num_blocks,
                            int32_t* error_count, hipStream_t stream);
