@@ -14,6 +14,8 @@ Cache (each replica holds identical values). Prints one JSON line.
     python bench.py --copy-calibration     # plain copy of known size, for rocprofv3 --pmc
     python bench.py --op kv_swap_out|kv_swap_in|kv_copy_d2d|kv_append   # cache operations
     python bench.py --op cpu_decode [--cpu-threads N] [--cpu-isa ...]   # host-CPU attention
+    python bench.py --op profile_costs [--out F]   # T_ga / T_ca grids for the cost model
+    python bench.py --op schedule_sim [--costs F]  # load-aware scheduler vs GPU-only, simulated
 """
 from __future__ import annotations
 
@@ -335,6 +337,143 @@ def bench_cpu_decode(args, neo, W):
     return 0
 
 
+COST_AXES = {"b": [1, 4, 16, 64, 256, 1024], "s": [2048, 16384, 131072, 524288]}
+COST_SHAPE = {"num_q_heads": 32, "num_kv_heads": 8, "head_dim": 128, "block_size": 16}
+DEFAULT_COSTS = os.path.join(ROOT, "paper_2411_01142_amd", "cost_profiles",
+                             "mi355x_epyc16__llama3-8b_attention.json")
+
+
+def bench_profile_costs(args, torch, neo):
+    """Per-layer decode-attention time of the GPU path (T_ga) and of the CPU path
+    (T_ca) on a grid of (requests, total context tokens): the offline profile of
+    the cost model (Sec. 3.2). Each point is a batch of equal-length requests
+    over shuffled blocks of one pool of N(0,1) bf16 K/V."""
+    import numpy as np
+    hq, hkv, D, bs = (COST_SHAPE[k] for k in ("num_q_heads", "num_kv_heads", "head_dim",
+                                               "block_size"))
+    B_axis, S_axis = COST_AXES["b"], COST_AXES["s"]
+    nb_pool = max(S_axis) // bs + max(B_axis)
+    log(f"[bench] cost profile: pool {nb_pool} blocks, grid {len(B_axis)} x {len(S_axis)}")
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    k = torch.randn((nb_pool, hkv, D // 8, bs, 8), generator=gen, device="cuda").to(torch.bfloat16)
+    v = torch.randn((nb_pool, hkv, D, bs), generator=gen, device="cuda").to(torch.bfloat16)
+    k_host = k.view(torch.int16).cpu().numpy().view(np.uint16)
+    v_host = v.view(torch.int16).cpu().numpy().view(np.uint16)
+    perm = np.random.default_rng(7).permutation(nb_pool).astype(np.int32)
+    threads = args.cpu_threads or neo.cpu_default_threads()
+    hip = HipEvents()
+    sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    gpu_t, cpu_t = [], []
+    for B in B_axis:
+        grow, crow = [], []
+        for S in S_axis:
+            lens = np.full(B, S // B, np.int32)
+            lens[: S % B] += 1
+            nbs = (lens + bs - 1) // bs
+            mbps = int(nbs.max())
+            table = np.full((B, mbps), -1, np.int32)
+            o = 0
+            for b in range(B):
+                table[b, : nbs[b]] = perm[o: o + nbs[b]]
+                o += nbs[b]
+            q = torch.randn((B, hq, D), generator=gen, device="cuda").to(torch.bfloat16)
+            bt = torch.from_numpy(table).to("cuda")
+            sl = torch.from_numpy(lens).to("cuda")
+            ws = neo.new_workspace(B, hq, hkv)
+            out = torch.empty((B, hq, D), dtype=torch.float32, device="cuda")
+            for _ in range(3):
+                neo.decode_attention(q, k, v, bt, sl, out=out, workspace=ws)
+            torch.cuda.synchronize()
+            a, e = hip.create(), hip.create()
+            reps = 20
+            hip.record(a, sh)
+            for _ in range(reps):
+                neo.decode_attention(q, k, v, bt, sl, out=out, workspace=ws)
+            hip.record(e, sh)
+            torch.cuda.synchronize()
+            grow.append(hip.elapsed_ms(a, e) / reps * 1e-3)
+            hip.destroy(a)
+            hip.destroy(e)
+            qh = q.view(torch.int16).cpu().numpy().view(np.uint16)
+            oh = np.empty((B, hq, D), np.float32)
+            neo.cpu_decode_attention(qh, k_host, v_host, table, lens, out=oh, num_threads=threads)
+            ts = []
+            for _ in range(5):
+                t0 = time.perf_counter()
+                neo.cpu_decode_attention(qh, k_host, v_host, table, lens, out=oh,
+                                         num_threads=threads)
+                ts.append(time.perf_counter() - t0)
+            crow.append(sorted(ts)[2])
+            log(f"[bench]   B={B} S={S}: T_ga {grow[-1] * 1e6:.1f} us, T_ca {crow[-1] * 1e6:.1f} us")
+        gpu_t.append(grow)
+        cpu_t.append(crow)
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    prof = {"what": "per-layer decode-attention seconds, GPU path (t_ga) and CPU path (t_ca), "
+                    "on a grid of (requests b, total context tokens s); equal-length requests",
+            "shape": COST_SHAPE, "b": B_axis, "s": S_axis, "t_ga": gpu_t, "t_ca": cpu_t,
+            "gpu": torch.cuda.get_device_name(0), "cpu": cpu_model, "cpu_threads": threads,
+            "cpu_isa": neo.cpu_best_isa(), "command": "python3 bench.py --op profile_costs"}
+    if args.out:
+        with open(args.out, "w") as f:
+            json.dump(prof, f, indent=1)
+    print(json.dumps({"metric": "cost profile", "op": "profile_costs", **prof}), flush=True)
+    return 0
+
+
+def bench_schedule_sim(args):
+    """The load-aware scheduler against GPU-only scheduling, simulated over a
+    synthetic request mix with the measured attention costs (T_ga, T_ca) and a
+    synthetic linear stage for a Llama-3-8B-shaped layer on MI355X
+    (max(436 MB of weights / 6 TB/s, 2 x 218 M params x tokens / 1.75 PFLOP/s))."""
+    import random
+    from paper_2411_01142_amd import sched as S
+    with open(args.costs or DEFAULT_COSTS) as f:
+        prof = json.load(f)
+    ga = S.CostGrid(prof["b"], prof["s"], prof["t_ga"])
+    ca = S.CostGrid(prof["b"], prof["s"], prof["t_ca"])
+    xs = [1.0, 64.0, 256.0, 1024.0, 8192.0]
+    tl = S.CostCurve(xs, [max(436e6 / 6e12, 2 * 218e6 * x / 1.75e15) for x in xs])
+    rng = random.Random(args.seed or 0)
+    reqs = [(i, rng.randint(64, 2048), rng.randint(16, 512)) for i in range(2000)]
+    results = {}
+    # GPU KV cache for 16 K tokens per layer-set (a memory-bound regime) and a
+    # CPU cache 16x larger; the GPU-only baseline preempts instead of swapping.
+    for policy, cpu_blocks in (("neo", 16384), ("gpu_only", 0)):
+        sc = S.Scheduler(S.SchedConfig(num_layers=32, block_size=16, gpu_blocks=1024,
+                                       cpu_blocks=cpu_blocks, max_batch_tokens=8192, t_ga=ga,
+                                       t_ca=ca, t_l=tl, policy=policy))
+        for r in reqs:
+            sc.add(*r)
+        t0 = time.perf_counter()
+        its = sc.run()
+        wall = time.perf_counter() - t0
+        st = sc.stats()
+        results[policy] = {"tokens_per_s": round(st["tokens"] / st["now"], 1),
+                           "iterations": st["iterations"],
+                           "two_batch_iterations": st["two_batch_iterations"],
+                           "swapped_out": st["swapped_out"], "swapped_in": st["swapped_in"],
+                           "preempted": st["preempted"],
+                           "scheduler_us_per_iteration": round(wall / max(1, len(its)) * 1e6, 2)}
+    out = {"metric": "simulated decode throughput, load-aware scheduler vs GPU-only",
+           "op": "schedule_sim", "unit": "tokens/s (simulated)",
+           "value": results["neo"]["tokens_per_s"],
+           "gain": round(results["neo"]["tokens_per_s"] / results["gpu_only"]["tokens_per_s"], 4),
+           "results": results,
+           "config": {"workload": "2000 requests, prompt U[64,2048], output U[16,512], all at t=0; "
+                                  "32 layers; GPU KV 1024 blocks x 16 tokens, CPU KV 16384 blocks",
+                      "costs": os.path.relpath(args.costs or DEFAULT_COSTS, ROOT),
+                      "gpu": prof.get("gpu"), "cpu": prof.get("cpu")}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -351,7 +490,9 @@ def main(argv=None):
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--op", default="decode",
                     choices=["decode", "kv_swap_out", "kv_swap_in", "kv_copy_d2d", "kv_append",
-                             "cpu_decode"])
+                             "cpu_decode", "profile_costs", "schedule_sim"])
+    ap.add_argument("--out", default="")
+    ap.add_argument("--costs", default="")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--cpu-isa", default="auto",
                     choices=["auto", "generic", "avx512", "avx512_bf16"])
@@ -362,6 +503,8 @@ def main(argv=None):
               "collective, and the benchmark runs on a single MI355X (--gpus 1).", file=sys.stderr)
         return 2
 
+    if args.op == "schedule_sim":
+        return bench_schedule_sim(args)
     if args.op == "cpu_decode":
         import paper_2411_01142_amd as neo
         from paper_2411_01142_amd import workloads as W
@@ -375,6 +518,8 @@ def main(argv=None):
     import paper_2411_01142_amd as neo
     from paper_2411_01142_amd import workloads as W
 
+    if args.op == "profile_costs":
+        return bench_profile_costs(args, torch, neo)
     if args.op != "decode":
         return bench_kv_op(args, torch, neo, W)
 

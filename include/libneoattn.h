@@ -257,6 +257,84 @@ int32_t neo_cpu_default_threads(void);
 neo_status neo_cpu_read_probe(const void* buf, size_t bytes, int32_t num_threads,
                               double* checksum);
 
+/* ------------------------------------------------------------------------
+ * Cost model and load-aware scheduler (Sec. 3.2), host only.
+ *
+ * Per-layer stage times are profiled offline and linearly interpolated:
+ * GPU decode attention T_ga and CPU decode attention T_ca on a grid of
+ * (requests in the sub-batch, their total context tokens), the linear stage
+ * T_l (pre- plus post-projection) on a curve over the sub-batch's tokens.
+ * Interpolation is bilinear inside the grid; outside it the edge cell's
+ * plane (line, for a curve) is extended; an axis of one point is constant.
+ * An empty sub-batch costs 0.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int32_t n_b, n_s;   /* axis lengths, >= 1 */
+  const double* b;    /* [n_b] requests, strictly ascending */
+  const double* s;    /* [n_s] total context tokens, strictly ascending */
+  const double* t;    /* [n_b][n_s] seconds per layer */
+} neo_cost_grid;
+
+typedef struct {
+  int32_t n;          /* >= 1 */
+  const double* x;    /* [n] tokens, strictly ascending */
+  const double* t;    /* [n] seconds per layer */
+} neo_cost_curve;
+
+/* Interpolated value of a grid at (b, s) / of a curve at x. */
+neo_status neo_cost_eval_grid(const neo_cost_grid* grid, double b, double s, double* out);
+neo_status neo_cost_eval_curve(const neo_cost_curve* curve, double x, double* out);
+
+typedef enum { NEO_SCHED_POLICY_NEO = 0, NEO_SCHED_POLICY_GPU_ONLY = 1 } neo_sched_policy;
+typedef enum { NEO_SCHED_GPU_ONLY = 0, NEO_SCHED_TWO_BATCH = 1 } neo_sched_mode;
+
+typedef struct {
+  int32_t num_layers;              /* L of the iteration-time model */
+  int32_t block_size;              /* tokens per KV block */
+  int64_t gpu_blocks;              /* GPU KV cache capacity, blocks */
+  int64_t cpu_blocks;              /* CPU KV cache capacity, blocks (0: no offloading) */
+  int64_t max_batch_tokens;        /* activation capacity: tokens of both sub-batches' linear stages */
+  int64_t swap_in_reserve_blocks;  /* GPU blocks left free after a swap-in */
+  neo_cost_grid t_ga, t_ca;        /* copied at creation */
+  neo_cost_curve t_l;              /* copied at creation */
+  int32_t policy;                  /* neo_sched_policy: NEO = the six steps; GPU_ONLY = steps 1-3 */
+} neo_sched_config;
+
+/* One iteration's decision. ids (if given) receives, in order, the request
+ * ids of: prefills, GPU decodes, CPU decodes in batch-0, CPU decodes in
+ * batch-1 (both only for TWO_BATCH), swap-outs, swap-ins. */
+typedef struct {
+  int32_t done;                    /* 1: no request left; nothing else is set */
+  int32_t mode;                    /* neo_sched_mode chosen */
+  int32_t n_prefill, n_prefill_to_cpu, n_gpu_decode, n_cpu_decode0, n_cpu_decode1;
+  int32_t n_swap_out, n_swap_in;
+  int64_t n_tokens;                /* tokens produced (one per scheduled request) */
+  double t_iter;                   /* estimated time of the chosen schedule, s */
+  double t_two_batch, t_gpu_only;  /* both estimates */
+  double t_l0, t_l1, t_ga0, t_ca0, t_ca1;  /* per-layer stage estimates of the two-batch schedule */
+  double now;                      /* simulated time after the iteration */
+} neo_sched_iter;
+
+typedef struct {
+  double now;
+  int64_t tokens, iterations, two_batch_iterations, finished;
+  int64_t swapped_out, swapped_in, preempted;
+  int64_t gpu_blocks_held, cpu_blocks_held, waiting, gpu_running, cpu_running;
+} neo_sched_stats;
+
+typedef struct neo_sched neo_sched;
+
+/* A simulator of the load-aware scheduler: each neo_sched_step makes one
+ * iteration's schedule in the six steps of Sec. 3.2 and advances every
+ * scheduled request by one token, simulated time by the estimate. */
+neo_status neo_sched_create(const neo_sched_config* cfg, neo_sched** out);
+/* Requests enter the prefill wait queue at `arrival` (simulated seconds). */
+neo_status neo_sched_add_request(neo_sched* s, int64_t id, int32_t prompt_len, int32_t output_len,
+                                 double arrival);
+neo_status neo_sched_step(neo_sched* s, neo_sched_iter* info, int64_t* ids, int64_t ids_capacity);
+neo_status neo_sched_get_stats(const neo_sched* s, neo_sched_stats* out);
+void neo_sched_destroy(neo_sched* s);
+
 /*
  * Opt-in check of the indexing inputs: counts seq_lens outside
  * [0, max_blocks_per_seq * block_size] and block-table entries in use

@@ -17,7 +17,7 @@ BUILD_DIR = os.path.join(PKG, "_build")
 SOURCES = ["api.hip", "plan_combine.hip", "decode_mfma.hip", "decode_valu.hip", "kv_ops.hip"]
 # Host-only C++ (the CPU attention), built with the host compiler; its
 # ISA-specific functions carry target attributes and are picked at run time.
-HOST_SOURCES = ["cpu_attention.cpp"]
+HOST_SOURCES = ["cpu_attention.cpp", "scheduler.cpp"]
 HOST_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-pthread", "-fno-math-errno",
               "-I" + INCLUDE, "-I" + CSRC]
 

@@ -257,11 +257,16 @@ void task_generic(const Problem& P, const Task& t) {
 
 enum class Math { kDot, kFma };
 
-// 2^x for x <= 0 (x = -inf gives 0): x = n + f with n = round(x), |f| <= 1/2,
-// 2^f = e^(f ln 2) by its Taylor series to degree 7 (remainder below 6e-9
-// relative), then scaled by 2^n.
+// 2^x for x <= 0: x = n + f with n = round(x), |f| <= 1/2, 2^f = e^(f ln 2)
+// by its Taylor series to degree 7 (remainder below 6e-9 relative), then
+// scaled by 2^n. Below x = -125 the result is 0 (x = -inf included): a weight
+// that far under the running maximum changes nothing in fp32, and it keeps
+// every intermediate a normal number (denormals take slow microcode assists
+// on some cores).
 NEO_AVX512 inline __m512 exp2_ps(__m512 x) {
-  x = _mm512_max_ps(x, _mm512_set1_ps(-160.f));
+  const __m512 lo = _mm512_set1_ps(-125.f);
+  const __mmask16 keep = _mm512_cmp_ps_mask(x, lo, _CMP_GE_OQ);
+  x = _mm512_max_ps(x, lo);
   const __m512 n = _mm512_roundscale_ps(x, _MM_FROUND_TO_NEAREST_INT | _MM_FROUND_NO_EXC);
   const __m512 f = _mm512_sub_ps(x, n);
   constexpr double c1 = 0.6931471805599453;  // ln 2
@@ -275,7 +280,7 @@ NEO_AVX512 inline __m512 exp2_ps(__m512 x) {
   p = _mm512_fmadd_ps(p, f, _mm512_set1_ps((float)c2));
   p = _mm512_fmadd_ps(p, f, _mm512_set1_ps((float)c1));
   p = _mm512_fmadd_ps(p, f, _mm512_set1_ps(1.f));
-  return _mm512_scalef_ps(p, n);
+  return _mm512_maskz_mov_ps(keep, _mm512_scalef_ps(p, n));
 }
 
 // 32 bf16 (as 16 dwords) -> fp32 of the even elements / of the odd elements.
@@ -379,19 +384,21 @@ NEO_AVX512 inline void score_tile_fma(const uint16_t* kt, const float* const* qs
 // V tile rows (2dp, 2dp + 1) are the 64 bytes at element dp * 32. acc[h][dp]
 // lanes 0-7 gather row 2dp, lanes 8-15 row 2dp+1 (token pairs), reduced at
 // the end of the task. One call: d pairs [4 db, 4 db + 4), heads [h0, h0+HB),
-// all tiles of the chunk; the stored accumulators are first scaled by alpha.
+// all tiles of the chunk; the stored accumulators are first scaled by alpha
+// (on the task's first chunk, `fresh`, they start from zero instead).
 // P per (head, tile): kDot: 16 bf16 hi then 16 bf16 lo (64 bytes);
 // kFma: 8 fp32 weights of even tokens then 8 of odd tokens (64 bytes).
 template <int HB>
 NEO_AVX512BF16 inline void accumulate_v_dot(const uint16_t* const* vtiles, int ntiles, int db,
                                             const uint8_t* pbuf, int h0, float* accv,
-                                            const float* alpha) {
+                                            const float* alpha, bool fresh) {
   __m512 acc[HB][4];
 #pragma GCC unroll 4
   for (int h = 0; h < HB; ++h) {
     const __m512 a = _mm512_set1_ps(alpha[h0 + h]);
     for (int i = 0; i < 4; ++i)
-      acc[h][i] = _mm512_mul_ps(_mm512_load_ps(accv + ((h0 + h) * 64 + db * 4 + i) * 16), a);
+      acc[h][i] = fresh ? _mm512_setzero_ps()
+                        : _mm512_mul_ps(_mm512_load_ps(accv + ((h0 + h) * 64 + db * 4 + i) * 16), a);
   }
   for (int tt = 0; tt < ntiles; ++tt) {
     const uint16_t* vt = vtiles[tt] + db * 4 * 32;
@@ -423,13 +430,14 @@ NEO_AVX512BF16 inline void accumulate_v_dot(const uint16_t* const* vtiles, int n
 template <int HB>
 NEO_AVX512 inline void accumulate_v_fma(const uint16_t* const* vtiles, int ntiles, int db,
                                         const uint8_t* pbuf, int h0, float* accv,
-                                        const float* alpha) {
+                                        const float* alpha, bool fresh) {
   __m512 acc[HB][4];
 #pragma GCC unroll 4
   for (int h = 0; h < HB; ++h) {
     const __m512 a = _mm512_set1_ps(alpha[h0 + h]);
     for (int i = 0; i < 4; ++i)
-      acc[h][i] = _mm512_mul_ps(_mm512_load_ps(accv + ((h0 + h) * 64 + db * 4 + i) * 16), a);
+      acc[h][i] = fresh ? _mm512_setzero_ps()
+                        : _mm512_mul_ps(_mm512_load_ps(accv + ((h0 + h) * 64 + db * 4 + i) * 16), a);
   }
   for (int tt = 0; tt < ntiles; ++tt) {
     const uint16_t* vt = vtiles[tt] + db * 4 * 32;
@@ -453,6 +461,20 @@ NEO_AVX512 inline void accumulate_v_fma(const uint16_t* const* vtiles, int ntile
   for (int h = 0; h < HB; ++h)
     for (int i = 0; i < 4; ++i)
       _mm512_store_ps(accv + ((h0 + h) * 64 + db * 4 + i) * 16, acc[h][i]);
+}
+
+// fp32 query in the kFma order: per piece c, dims (8c, 8c+2, 8c+4, 8c+6)
+// then (8c+1, 8c+3, 8c+5, 8c+7). 64 bytes of bf16 (pieces 4k..4k+3) widen to
+// even and odd dims, interleaved four at a time.
+NEO_AVX512 inline void split_query(const uint16_t* q, float* out) {
+  const __m512i lo = _mm512_set_epi32(23, 22, 21, 20, 7, 6, 5, 4, 19, 18, 17, 16, 3, 2, 1, 0);
+  const __m512i hi = _mm512_set_epi32(31, 30, 29, 28, 15, 14, 13, 12, 27, 26, 25, 24, 11, 10, 9, 8);
+  for (int k = 0; k < 4; ++k) {
+    const __m512i x = _mm512_loadu_si512(q + 32 * k);
+    const __m512 e = even_ps(x), o = odd_ps(x);
+    _mm512_store_ps(out + 32 * k, _mm512_permutex2var_ps(e, lo, o));
+    _mm512_store_ps(out + 32 * k + 16, _mm512_permutex2var_ps(e, hi, o));
+  }
 }
 
 // P of one (head, tile) from its 16 base-2 scores and the running max.
@@ -492,17 +514,12 @@ NEO_AVX512 inline __m512 store_p_fma(__m512 s, __m512 mv, uint8_t* pp) {
   for (int h = 0; h < G; ++h) {                                                              \
     qrow[h] = P.q + ((size_t)t.b * P.hq + (size_t)t.g * G + h) * kD;                         \
     if (M == Math::kFma) {                                                                   \
-      for (int c = 0; c < 16; ++c)                                                           \
-        for (int r = 0; r < 4; ++r) {                                                        \
-          qsplit[h][c * 8 + r] = bf16_to_f32(qrow[h][8 * c + 2 * r]);                        \
-          qsplit[h][c * 8 + 4 + r] = bf16_to_f32(qrow[h][8 * c + 2 * r + 1]);                \
-        }                                                                                    \
+      split_query(qrow[h], qsplit[h]);                                                       \
       qs[h] = qsplit[h];                                                                     \
     }                                                                                        \
     m[h] = -INFINITY;                                                                        \
     l[h] = 0.f;                                                                              \
   }                                                                                          \
-  memset(accv, 0, sizeof accv);                                                              \
   const int32_t* row = P.table + (size_t)t.b * P.mbps;                                       \
   for (int jc = t.j0; jc < t.j1; jc += kChunk) {                                             \
     const int n = std::min(kChunk, t.j1 - jc);                                               \
@@ -521,12 +538,14 @@ NEO_AVX512 inline __m512 store_p_fma(__m512 s, __m512 mv, uint8_t* pp) {
           score_tile_fma<HB>(P.k + tile, qs + h0, valid, P.scale_log2, so);                  \
       }                                                                                      \
       if (valid < kBs) {                                                                     \
-        /* unused slots of the last tile: weight 0, but 0 * NaN must not reach P*V */        \
-        const __mmask16 live = (__mmask16)((1u << valid) - 1);                               \
-        for (int d = 0; d < kD; ++d)                                                         \
-          _mm256_store_si256((__m256i*)(vtail + d * kBs),                                    \
-                             _mm256_maskz_mov_epi16(live, _mm256_loadu_si256(                \
-                                 (const __m256i*)(P.v + tile + d * kBs))));                  \
+        /* unused slots of the last tile: weight 0, but 0 * NaN must not reach P*V. */      \
+        /* Two dims per 64-byte store, the size P*V loads, so the loads are forwarded. */    \
+        const uint32_t live16 = (1u << valid) - 1;                                           \
+        const __mmask32 live = (__mmask32)(live16 | (live16 << 16));                         \
+        for (int d = 0; d < kD; d += 2)                                                      \
+          _mm512_store_si512(vtail + d * kBs,                                                \
+                             _mm512_maskz_mov_epi16(live, _mm512_loadu_si512(                \
+                                 P.v + tile + d * kBs)));                                    \
         vtiles[tt] = vtail;                                                                  \
       }                                                                                      \
     }                                                                                        \
@@ -548,9 +567,9 @@ NEO_AVX512 inline __m512 store_p_fma(__m512 s, __m512 mv, uint8_t* pp) {
     for (int db = 0; db < 16; ++db)                                                          \
       for (int h0 = 0; h0 < G; h0 += HB) {                                                   \
         if (M == Math::kDot)                                                                 \
-          accumulate_v_dot<HB>(vtiles, n, db, pbuf, h0, accv, alpha);                        \
+          accumulate_v_dot<HB>(vtiles, n, db, pbuf, h0, accv, alpha, jc == t.j0);            \
         else                                                                                 \
-          accumulate_v_fma<HB>(vtiles, n, db, pbuf, h0, accv, alpha);                        \
+          accumulate_v_fma<HB>(vtiles, n, db, pbuf, h0, accv, alpha, jc == t.j0);            \
       }                                                                                      \
   }                                                                                          \
   for (int h = 0; h < G; ++h) {                                                              \
