@@ -222,6 +222,14 @@ neo_status neo_cpu_decode_attention(const void* q, const void* k_cache, const vo
                                     int32_t max_blocks_per_seq, int32_t num_blocks,
                                     int32_t num_threads);
 
+/* neo_kv_append for a cache in host memory, on the calling thread (the CPU
+ * side of a CPU-request's decode step). Same arguments, layouts and rules;
+ * every pointer is host memory; synchronous. */
+neo_status neo_cpu_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                             const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                             int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                             int32_t block_size, int32_t num_blocks);
+
 /* Instruction-set paths of the CPU attention. */
 typedef enum {
   NEO_CPU_ISA_AUTO = 0,        /* the best this CPU supports */

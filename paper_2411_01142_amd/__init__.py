@@ -28,7 +28,7 @@ __all__ = [
     "NeoError", "decode_attention", "workspace_bytes", "paged_gather", "debug_validate",
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
     "new_workspace", "kv_append", "copy_blocks", "cpu_decode_attention", "CPU_ISAS",
-    "cpu_best_isa", "cpu_default_threads", "cpu_read_probe",
+    "cpu_best_isa", "cpu_default_threads", "cpu_read_probe", "cpu_kv_append",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -99,6 +99,8 @@ def load_library():
         lib.neo_cpu_decode_attention_ex.restype = ctypes.c_int
         lib.neo_cpu_decode_attention.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I]
         lib.neo_cpu_decode_attention.restype = ctypes.c_int
+        lib.neo_cpu_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I]
+        lib.neo_cpu_kv_append.restype = ctypes.c_int
         lib.neo_cpu_read_probe.argtypes = [P, ctypes.c_size_t, I, ctypes.POINTER(ctypes.c_double)]
         lib.neo_cpu_read_probe.restype = ctypes.c_int
         lib.neo_cpu_best_isa.argtypes = []
@@ -415,3 +417,22 @@ def cpu_read_probe(buf, num_threads: int = 0) -> float:
     _check(load_library().neo_cpu_read_probe(buf.ctypes.data, buf.nbytes, int(num_threads),
                                              ctypes.byref(out)))
     return out.value
+
+
+def cpu_kv_append(k_cache, v_cache, k_new, v_new, block_table, seq_lens):
+    """``kv_append`` for host-memory caches (numpy uint16 bit patterns or CPU bf16
+    tensors), on the calling thread."""
+    import numpy as np
+    lib = load_library()
+    kp, _ = _host_array(k_cache, "k_cache", np.uint16, 5)
+    vp, _ = _host_array(v_cache, "v_cache", np.uint16, 4)
+    knp, _ = _host_array(k_new, "k_new", np.uint16, 3)
+    vnp, _ = _host_array(v_new, "v_new", np.uint16, 3)
+    bp, _ = _host_array(block_table, "block_table", np.int32, 2)
+    lp, _ = _host_array(seq_lens, "seq_lens", np.int32, 1)
+    NB, Hkv, npieces, bs, x = k_cache.shape
+    B = seq_lens.shape[0]
+    if tuple(k_new.shape) != (B, Hkv, npieces * x) or tuple(v_new.shape) != tuple(k_new.shape):
+        raise ValueError("k_new and v_new must be [batch, num_kv_heads, head_dim]")
+    _check(lib.neo_cpu_kv_append(kp, vp, knp, vnp, bp, lp, B, block_table.shape[1], Hkv,
+                                 npieces * x, bs, NB))

@@ -821,6 +821,45 @@ neo_status neo_cpu_read_probe(const void* buf, size_t bytes, int32_t num_threads
 
 int32_t neo_cpu_best_isa(void) { return neo::cpu::best_isa(); }
 
+neo_status neo_cpu_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                             const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
+                             int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
+                             int32_t block_size, int32_t num_blocks) {
+  using neo::set_error;
+  namespace C = neo::cpu;
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (num_kv_heads <= 0) return set_error(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
+  if (head_dim != C::kD || block_size != C::kBs)
+    return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
+                     head_dim, block_size);
+  if (batch == 0) return neo::clear_error();
+  if (!k_cache || !v_cache || !k_new || !v_new || !block_table || !seq_lens)
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  uint16_t* kc = static_cast<uint16_t*>(k_cache);
+  uint16_t* vc = static_cast<uint16_t*>(v_cache);
+  const uint16_t* kn = static_cast<const uint16_t*>(k_new);
+  const uint16_t* vn = static_cast<const uint16_t*>(v_new);
+  for (int64_t b = 0; b < batch; ++b) {
+    const int32_t L = C::clamp_len(seq_lens[b], max_blocks_per_seq);
+    if (L <= 0) continue;
+    const int32_t t = L - 1;
+    const int32_t blk = block_table[b * max_blocks_per_seq + t / C::kBs];
+    if (blk < 0 || blk >= num_blocks) continue;
+    const int slot = t % C::kBs;
+    for (int64_t g = 0; g < num_kv_heads; ++g) {
+      const size_t tile = ((size_t)blk * num_kv_heads + g) * C::kTile;
+      const uint16_t* ks = kn + ((size_t)b * num_kv_heads + g) * C::kD;
+      const uint16_t* vs = vn + ((size_t)b * num_kv_heads + g) * C::kD;
+      for (int c = 0; c < C::kD / 8; ++c)
+        memcpy(kc + tile + ((size_t)c * C::kBs + slot) * 8, ks + c * 8, 16);
+      for (int d = 0; d < C::kD; ++d) vc[tile + (size_t)d * C::kBs + slot] = vs[d];
+    }
+  }
+  return neo::clear_error();
+}
+
 int32_t neo_cpu_default_threads(void) { return neo::cpu::default_threads(); }
 
 neo_status neo_cpu_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,

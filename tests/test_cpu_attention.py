@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 import paper_2411_01142_amd as neo
+from kv_cases import drop_last_tokens
 from paper_2411_01142_amd import workloads as W
 
 ABS_TOL = 1e-2
@@ -216,3 +217,27 @@ def test_read_probe_sums_the_buffer():
     assert neo.cpu_read_probe(buf, 3) == pytest.approx(float(buf.sum()), rel=1e-6)
     with pytest.raises(neo.NeoError):
         neo.cpu_read_probe(np.ones(10, np.float32))
+
+
+@pytest.mark.parametrize("hkv", [1, 2, 8])
+def test_cpu_append_restores_the_dropped_token(hkv):
+    case = W.build_case([1, 5, 16, 17, 40, 0, 33], 2 * hkv, hkv, 128, 16, seed=hkv)
+    dropped, k_new, v_new = drop_last_tokens(case)
+    neo.cpu_kv_append(dropped.k_cache, dropped.v_cache, k_new, v_new, case.block_table,
+                      case.seq_lens)
+    assert np.array_equal(dropped.k_cache, case.k_cache)
+    assert np.array_equal(dropped.v_cache, case.v_cache)
+
+
+def test_cpu_append_matches_oracle_with_clamps_and_bad_ids():
+    case = W.build_case([20, 9, 16, 0], 2, 1, 128, 16, seed=6)
+    case.seq_lens[:] = [20, 9, 1000, 0]
+    case.block_table[2, 1] = 1
+    case.block_table[1, 0] = case.num_blocks + 3
+    rng = np.random.default_rng(4)
+    k_new = rng.integers(0, 1 << 16, size=(4, 1, 128), dtype=np.uint16)
+    v_new = rng.integers(0, 1 << 16, size=(4, 1, 128), dtype=np.uint16)
+    k, v = case.k_cache.copy(), case.v_cache.copy()
+    neo.cpu_kv_append(k, v, k_new, v_new, case.block_table, case.seq_lens)
+    oracle.kv_append(case, k_new, v_new)
+    assert np.array_equal(k, case.k_cache) and np.array_equal(v, case.v_cache)
