@@ -609,7 +609,7 @@ def main(argv=None):
     sh = ctypes.c_void_p(stream.cuda_stream)
     variant_id = neo.VARIANTS[args.variant]
     schedule_id = neo.SCHEDULES[args.schedule]
-    schedule = "two_kernel" if args.schedule == "auto" else args.schedule
+    schedule = "fused" if args.schedule == "auto" else args.schedule
     resolved = "mfma" if args.variant == "auto" else args.variant
     hip = HipEvents()
     ev = [(hip.create(), hip.create()) for _ in range(args.steps)]

@@ -79,7 +79,7 @@ typedef enum {
 
 /* How the call is launched (neo_decode_attention_ex). */
 typedef enum {
-  NEO_SCHEDULE_AUTO = 0,       /* two-kernel (the fastest on MI355X for every length mix tried) */
+  NEO_SCHEDULE_AUTO = 0,       /* fused (equal or fastest on MI355X for every length mix tried) */
   NEO_SCHEDULE_FUSED = 1,      /* one kernel: each wavefront plans its own slice from seq_lens
                                   and the last slice to finish a split request merges it */
   NEO_SCHEDULE_STAGED = 2,     /* three kernels: plan, decode, log-sum-exp combine */

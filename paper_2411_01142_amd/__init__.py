@@ -185,9 +185,9 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
     """Decode attention of the whole ragged batch; returns ``out`` (fp32 [B, Hq, 128]).
 
     ``scale`` defaults to 1/sqrt(head_dim). ``variant`` picks the kernel family
-    ("auto", "valu", "mfma"); ``schedule`` the launch ("auto"/"two_kernel":
-    decode then combine; "staged": plan, decode and combine; "fused": one
-    kernel); ``max_slices`` caps
+    ("auto", "valu", "mfma"); ``schedule`` the launch ("auto"/"fused": one
+    kernel; "two_kernel": decode then combine; "staged": plan, decode and
+    combine); ``max_slices`` caps
     the sequence slices of the plan (0 = library default, 1 = never split a
     request). ``workspace`` (a zero-filled uint8 GPU tensor of at least
     ``workspace_bytes(...)``, see ``new_workspace``) is allocated and cached per

@@ -190,12 +190,13 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
       max_slices == 0 ? std::min<int32_t>(2 * quantum, NEO_MAX_SLICES) : max_slices;
   const int32_t min_tiles = max_slices == 0 ? 0 : 1;
   if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
-  // Default: decode (planning in-wave) + combine. Measured on MI355X it beats
-  // the three-kernel launch (one launch and one plan read fewer) and the fused
-  // kernel (whose in-kernel merges cost more than a short combine launch).
-  const neo::Schedule sched = schedule == NEO_SCHEDULE_FUSED    ? neo::kFused
-                              : schedule == NEO_SCHEDULE_STAGED ? neo::kStaged
-                                                                : neo::kTwoKernel;
+  // Default: the fused kernel. Any launch costs ~4.6 us on MI355X, so the
+  // combine launch of the two-kernel schedule (~6 us) outweighs the in-kernel
+  // merges at the end of the fused one; measured equal or faster on every
+  // length mix tried.
+  const neo::Schedule sched = schedule == NEO_SCHEDULE_TWO_KERNEL ? neo::kTwoKernel
+                              : schedule == NEO_SCHEDULE_STAGED   ? neo::kStaged
+                                                                  : neo::kFused;
 
   char* ws = static_cast<char*>(workspace);
   neo::DecodeParams p;

@@ -39,8 +39,24 @@ constexpr float kLn2 = 0.6931471805599453f;
 __device__ inline void store_coherent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Two adjacent floats (8-byte aligned) in one coherent store.
+__device__ inline void store_coherent2(float* p, float a, float b) {
+  const uint64_t bits = (uint64_t)__builtin_bit_cast(uint32_t, a) |
+                        ((uint64_t)__builtin_bit_cast(uint32_t, b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), bits, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ inline float load_coherent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Two adjacent floats (8-byte aligned) in one coherent load.
+__device__ inline float2 load_coherent2(const float* p) {
+  const uint64_t bits = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+  float2 r;
+  r.x = __builtin_bit_cast(float, (uint32_t)bits);
+  r.y = __builtin_bit_cast(float, (uint32_t)(bits >> 32));
+  return r;
 }
 __device__ inline void wait_all_memory() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -210,6 +226,26 @@ __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwav
   }
 }
 
+// out rows of pair (b, g) from two contributors' log-sum-exps and rows (this
+// lane's two dims): the two-contributor case of merge_pair, operation for
+// operation.
+template <int G>
+__device__ inline void merge_two_values(const DecodeParams& p, int32_t b, int32_t g,
+                                        const float* la, const float* lb, const float2* oa,
+                                        const float2* ob, int lane) {
+  const int d = 2 * lane;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float m = fmaxf(la[h], lb[h]);
+    const float wa = __expf(la[h] - m), wb = __expf(lb[h] - m);
+    const float inv = 1.f / (wa + wb);
+    float2 r;
+    r.x = fmaf(wb, ob[h].x, wa * oa[h].x) * inv;
+    r.y = fmaf(wb, ob[h].y, wa * oa[h].y) * inv;
+    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
+  }
+}
+
 // Merge the partials of one cut pair into out[b][g*G .. g*G+G): with M the
 // largest log-sum-exp, out = sum_c e^(lse_c - M) o_c / sum_c e^(lse_c - M).
 // Contributors are slices c0..c1, taken 64 at a time with a running maximum
@@ -223,6 +259,9 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
                                   int32_t c0, int32_t c1, int32_t W, int32_t n, int lane) {
   constexpr int kBatch = 32 / G > 16 ? 16 : (32 / G > 0 ? 32 / G : 1);  // 64 registers
   auto ld = [](const float* a) -> float { return kCoherent ? load_coherent(a) : *a; };
+  auto ld2 = [](const float* a) -> float2 {
+    return kCoherent ? load_coherent2(a) : *reinterpret_cast<const float2*>(a);
+  };
   const int k = c1 - c0 + 1;
   const int d = 2 * lane;
   float m[G], z[G], a0[G], a1[G];
@@ -242,19 +281,24 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
         const int slot = partial_slot(c, slice_start(c, W, n), first_tile);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          const float* o = p.part_o + ((size_t)slot * G + h) * kHeadDim + d;
-          ov[u][h][0] = ld(o);
-          ov[u][h][1] = ld(o + 1);
+          const float2 v = ld2(p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
+          ov[u][h][0] = v.x;
+          ov[u][h][1] = v.y;
         }
       }
     };
     load_rows(0, true);
     const int mine = c0 + base + (lane < cnt ? lane : 0);
     const int my_slot = partial_slot(mine, slice_start(mine, W, n), first_tile);
+    // Every head's log-sum-exp is loaded before any cross-lane step, so the
+    // loads share one round trip.
+    float lse_h[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) lse_h[h] = ld(p.part_lse + my_slot * G + h);
     float w[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float lse = lane < cnt ? ld(p.part_lse + my_slot * G + h) : -INFINITY;
+      const float lse = lane < cnt ? lse_h[h] : -INFINITY;
       const float mc = fmaxf(m[h], wave_max_f32(lse));
       const float rescale = __expf(m[h] - mc);  // 0 on the first chunk
       a0[h] *= rescale;
@@ -286,6 +330,35 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
     r.y = a1[h] * inv;
     *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
   }
+}
+
+// The merge of a pair with exactly two contributors, partial slots sa (the
+// earlier slice) and sb, with every load in one round trip. Same arithmetic,
+// in the same order, as merge_pair for two contributors, so both give the
+// same bits.
+template <int G, bool kCoherent>
+__device__ inline void merge_two(const DecodeParams& p, int32_t b, int32_t g, int32_t sa,
+                                 int32_t sb, int lane) {
+  const int d = 2 * lane;
+  float la[G], lb[G];
+  float2 oa[G], ob[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float* pa = p.part_o + ((size_t)sa * G + h) * kHeadDim + d;
+    const float* pb = p.part_o + ((size_t)sb * G + h) * kHeadDim + d;
+    if (kCoherent) {
+      la[h] = load_coherent(p.part_lse + sa * G + h);
+      lb[h] = load_coherent(p.part_lse + sb * G + h);
+      oa[h] = load_coherent2(pa);
+      ob[h] = load_coherent2(pb);
+    } else {
+      la[h] = p.part_lse[sa * G + h];
+      lb[h] = p.part_lse[sb * G + h];
+      oa[h] = *reinterpret_cast<const float2*>(pa);
+      ob[h] = *reinterpret_cast<const float2*>(pb);
+    }
+  }
+  merge_two_values<G>(p, b, g, la, lb, oa, ob, lane);
 }
 
 // Fused launch: after writing its partial for a cut pair, a slice counts itself
@@ -350,10 +423,12 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   const size_t blk_stride = (size_t)p.hkv * kTileElems;
 
   // A slice holds at most two cut pairs: the one it starts in and the one it
-  // ends in. Their merges (fused launch) run after the tile loop.
+  // ends in. Their merges (fused launch) run after the tile loop. Two named
+  // records, not an array: a dynamically indexed array would be placed in LDS
+  // (measured: that allocation alone slows the whole kernel by ~15 %).
   struct Pending {
     int32_t b, g, first, c0, c1;
-  } pend[2];
+  } pend0{}, pend1{};
   int npend = 0;
 
   int32_t pos = si.s0;  // weighted position reached
@@ -424,11 +499,8 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         const int32_t c0 = slice_of(first_tile, si.W, si.n);
         const int32_t c1 = slice_of(first_tile + nb - 1, si.W, si.n);
         if (arrive_last(p, c0, c1, lane)) {
-          pend[npend].b = b;
-          pend[npend].g = g;
-          pend[npend].first = first_tile;
-          pend[npend].c0 = c0;
-          pend[npend].c1 = c1;
+          const Pending rec{b, g, first_tile, c0, c1};
+          if (npend == 0) pend0 = rec; else pend1 = rec;
           ++npend;
         }
       }
@@ -443,9 +515,16 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     }
   }
   if (kMergeHere) {
-    for (int i = 0; i < npend; ++i)
-      merge_pair<G, true>(p, pend[i].b, pend[i].g, pend[i].first, pend[i].c0, pend[i].c1, si.W,
-                          si.n, lane);
+    for (int i = 0; i < npend; ++i) {
+      const Pending q = i == 0 ? pend0 : pend1;
+      if (q.c1 == q.c0 + 1) {
+        merge_two<G, true>(p, q.b, q.g,
+                           partial_slot(q.c0, slice_start(q.c0, si.W, si.n), q.first),
+                           partial_slot(q.c1, slice_start(q.c1, si.W, si.n), q.first), lane);
+      } else {
+        merge_pair<G, true>(p, q.b, q.g, q.first, q.c0, q.c1, si.W, si.n, lane);
+      }
+    }
   }
 }
 

@@ -138,8 +138,8 @@ struct MfmaFamily {
       for (int mb = 0; mb < 8; ++mb) {
         const f32x4_t v = st.acc[mb] * inv;
         if (kCoherent) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) store_coherent(r + 16 * mb + i, v[i]);
+          store_coherent2(r + 16 * mb, v[0], v[1]);
+          store_coherent2(r + 16 * mb + 2, v[2], v[3]);
         } else {
           *reinterpret_cast<f32x4_t*>(r + 16 * mb) = v;
         }

@@ -103,11 +103,41 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeP
   const SliceStart a = p.starts[s];
   const int32_t W = p.hdr->total;
   const int32_t n = p.hdr->n_slices;
+  // A pair cut at this boundary nearly always has exactly two contributors:
+  // slice s-1's end-cut segment (slot 2s-1) and slice s's first segment (slot
+  // 2s). Their log-sum-exps and rows are loaded in the same round trip as the
+  // record (all slots exist whatever the plan; unused values are ignored).
+  // (s <= NEO_MAX_SLICES here; the slots read are clamped below 2 NEO_MAX_SLICES,
+  // s = NEO_MAX_SLICES being a boundary no plan has.)
+  const int d = 2 * lane;
+  const int sa = 2 * min(s, NEO_MAX_SLICES - 1) - 1, sb = sa + 1;
+  float la[G], lb[G];
+  float2 oa[G], ob[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    la[h] = p.part_lse[sa * G + h];
+    lb[h] = p.part_lse[sb * G + h];
+    oa[h] = *reinterpret_cast<const float2*>(p.part_o + ((size_t)sa * G + h) * kHeadDim + d);
+    ob[h] = *reinterpret_cast<const float2*>(p.part_o + ((size_t)sb * G + h) * kHeadDim + d);
+  }
+  // Every value above is an operand of this empty statement, so all the loads
+  // are issued before the branches below (left alone, the compiler moves the
+  // speculative ones after them, costing a second round trip).
+  asm volatile("" ::"v"(a.pos), "v"(a.x), "v"(a.nb), "s"(W), "s"(n));
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+    asm volatile("" ::"v"(la[h]), "v"(lb[h]), "v"(oa[h].x), "v"(oa[h].y), "v"(ob[h].x),
+                 "v"(ob[h].y));
   if (s >= n) return;
   if (a.x <= kPairCost) return;                 // no tile of the pair before the boundary
   const int32_t first_tile = a.pos - a.x + kPairCost;
-  if (first_tile < slice_start(s - 1, W, n)) return;  // an earlier boundary cuts it first
+  const int32_t prev_start = slice_start(s - 1, W, n);
+  if (first_tile < prev_start) return;          // an earlier boundary cuts it first
   const int32_t c1 = slice_of(first_tile + a.nb - 1, W, n);
+  if (c1 == s && first_tile > prev_start) {
+    merge_two_values<G>(p, a.b, a.g, la, lb, oa, ob, lane);  // slots 2s-1, 2s
+    return;
+  }
   merge_pair<G, false>(p, a.b, a.g, first_tile, s - 1, c1, W, n, lane);
 }
 
