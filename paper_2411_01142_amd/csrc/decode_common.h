@@ -434,8 +434,13 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   int32_t pos = si.s0;  // weighted position reached
   int b = si.b, g = si.g;
   int32_t x = si.x;     // offset of pos inside pair (b, g)
+  // Prefetched for the next pair while the current one streams: its
+  // request's length and first 64 block ids (request pf_b), so that a new
+  // pair's q and first tiles go out together instead of after two dependent
+  // round trips (length, then table row).
+  int32_t pf_b = -1, pf_L = 0, pf_vals = 0;
   while (b < p.batch) {
-    const int32_t L = clamp_len(p.lens[b], p.mbps);
+    const int32_t L = pf_b == b ? pf_L : clamp_len(p.lens[b], p.mbps);
     const int32_t nb = (L + kBlock - 1) / kBlock;
     if (nb == 0) {
       ++b;
@@ -452,7 +457,11 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // Block ids of this row, 64 at a time, one per lane.
     const int32_t* trow = p.table + (size_t)b * p.mbps;
     int32_t tbase = j;
-    int32_t tvals = (tbase + lane < jend) ? trow[tbase + lane] : 0;
+    int32_t tvals = (j == 0 && pf_b == b) ? pf_vals : ((tbase + lane < jend) ? trow[tbase + lane] : 0);
+    // The next pair is (b, g+1) or (b+1, 0); the next request's length is
+    // requested now and used after this pair's first tile loads are out.
+    const int32_t nq = g + 1 < p.hkv ? b : b + 1;
+    const int32_t lq_raw = (nq != b && nq < p.batch) ? p.lens[nq] : 0;
     auto tile_off = [&](int32_t jj) -> size_t {
       if (jj - tbase >= kWave) {
         tbase += kWave;
@@ -475,6 +484,32 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         const size_t off = tile_off(j + i);
         F::load_tile(buf[i], p.k + off, p.v + off, lane);
       }
+
+    // Prefetch for the next pair (in bounds: lanes below its block count,
+    // which is at most the table's row length).
+    if (nq < p.batch) {
+      const int32_t Lq = nq == b ? L : clamp_len(lq_raw, p.mbps);
+      const int32_t nbq = (Lq + kBlock - 1) / kBlock;
+      const int32_t* tq = p.table + (size_t)nq * p.mbps;
+      pf_vals = lane < min(nbq, kWave) ? tq[lane] : 0;
+      pf_b = nq;
+      pf_L = Lq;
+    }
+
+    // Fused launch, last pair of this slice cut with exactly one later slice
+    // (the next one), which handles its share of the pair first: if it has
+    // already arrived, this slice will be the last, so it merges straight
+    // from registers after its tiles (no partial of its own, no atomic, one
+    // round trip for the other partial). The counter is read here, after
+    // the first tile loads are out, and only looked at after the tiles.
+    bool merge_now = false;
+    if constexpr (kMergeHere && F::kFastMerge) {
+      if (j == 0 && jend < nb && slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1) {
+        const int32_t seen = __hip_atomic_load(p.counters + wave, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+        merge_now = __builtin_amdgcn_readfirstlane(seen) == 1;
+      }
+    }
     for (int32_t jj = j; jj < jend; jj += PF + 1) {
 #pragma unroll
       for (int u = 0; u <= PF; ++u) {
@@ -491,6 +526,15 @@ __device__ inline void decode_driver(const DecodeParams& p) {
 
     if (j == 0 && jend == nb) {
       F::template write<false>(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);
+    } else if (merge_now) {
+      if constexpr (kMergeHere && F::kFastMerge) {
+        if (lane == 0)
+          __hip_atomic_store(p.counters + wave, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int32_t nxt = wave + 1;
+        const int slot = partial_slot(nxt, slice_start(nxt, si.W, si.n), first_tile);
+        F::merge_write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
+                       p.out + ((size_t)b * p.hq + g * G) * kHeadDim, lane);
+      }
     } else {
       const int slot = partial_slot(wave, si.s0, first_tile);
       F::template write<kMergeHere>(st, p.part_o + (size_t)slot * G * kHeadDim,

@@ -43,6 +43,7 @@ struct MfmaFamily {
   struct Shared {
     int unused;
   };
+  static constexpr bool kFastMerge = true;  // provides merge_write
 
   __device__ static void load_q(Q& q, const uint16_t* __restrict__ qpair, int lane) {
     const int col = lane & 15, rq = lane >> 4;
@@ -150,10 +151,52 @@ struct MfmaFamily {
       }
     }
   }
+
+  // The pair's two-contributor merge done in registers: this slice's share
+  // (st, not yet written) first, then the other slice's complete partial
+  // (other_rows, other_lse, device-coherent loads); the same arithmetic as
+  // merge_two_values on the stored partials, so the output bits are the same.
+  __device__ static void merge_write(const State& st, const float* __restrict__ other_rows,
+                                     const float* __restrict__ other_lse,
+                                     float* __restrict__ out_rows, int lane) {
+    const int col = lane & 15, rq = lane >> 4;
+    float lt = st.l + __shfl_xor(st.l, 16);
+    lt += __shfl_xor(lt, 32);
+    const float inv = 1.f / lt;
+    if (col < G) {
+      // Rounded exactly as the stored log-sum-exp of write(): the empty asm
+      // makes la an opaque value, so the compiler cannot fuse its multiply
+      // with the subtraction of the max below (the merge must see the same
+      // value as the merge of stored partials).
+      float la = (st.m + __log2f(lt)) * kLn2;
+      asm volatile("" : "+v"(la));
+      const float lb = load_coherent(other_lse + col);
+      const float* ob = other_rows + col * kHeadDim + 4 * rq;
+      float2 o2[8][2];
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        o2[mb][0] = load_coherent2(ob + 16 * mb);
+        o2[mb][1] = load_coherent2(ob + 16 * mb + 2);
+      }
+      const float m = fmaxf(la, lb);
+      const float wa = __expf(la - m), wb = __expf(lb - m);
+      const float inv2 = 1.f / (wa + wb);
+      float* r = out_rows + col * kHeadDim + 4 * rq;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        const f32x4_t oa = st.acc[mb] * inv;
+        const float obv[4] = {o2[mb][0].x, o2[mb][0].y, o2[mb][1].x, o2[mb][1].y};
+        f32x4_t res;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) res[i] = fmaf(wb, obv[i], wa * oa[i]) * inv2;
+        *reinterpret_cast<f32x4_t*>(r + 16 * mb) = res;
+      }
+    }
+  }
 };
 
 template <int G, Schedule kSched>
-__global__ __launch_bounds__(kWave * kWavesPerGroup) void decode_mfma_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kWave * kWavesPerGroup, 2) void decode_mfma_kernel(DecodeParams p) {
   decode_driver<MfmaFamily<G>, G, 2, kSched>(p);
 }
 

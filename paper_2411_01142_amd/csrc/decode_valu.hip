@@ -66,6 +66,8 @@ struct ValuFamily {
   struct Shared {
     float p[G * kBlock];  // softmax weights of the current tile, [head][token]
   };
+  static constexpr bool kFastMerge = false;  // no merge_write: the general path merges
+
 
   __device__ static void load_q(Q& q, const uint16_t* __restrict__ qpair, int lane) {
     const int c = lane & 15;
