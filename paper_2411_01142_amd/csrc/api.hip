@@ -186,8 +186,10 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   st = device_cu_count(&cus);
   if (st != NEO_OK) return st;
   const int32_t quantum = cus * neo::kWavesPerGroup;
+  // Default: at most one slice per wave of one workgroup per CU (the policy
+  // in slice_count), so the grid has no workgroups without a slice.
   const int32_t slices =
-      max_slices == 0 ? std::min<int32_t>(2 * quantum, NEO_MAX_SLICES) : max_slices;
+      max_slices == 0 ? std::min<int32_t>(quantum, NEO_MAX_SLICES) : max_slices;
   const int32_t min_tiles = max_slices == 0 ? 0 : 1;
   if (variant == NEO_VARIANT_AUTO) variant = NEO_VARIANT_MFMA;
   // Default: the fused kernel. Any launch costs ~4.6 us on MI355X, so the

@@ -28,6 +28,37 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.6931471805599453f;
 
+// ----------------------------------------------------------------- tile loads
+
+// KV tiles are read through buffer resources covering one 4 KiB tile. A tile
+// past the end of a segment gets a resource of size 0: its loads still issue
+// (and count) but return zeros without touching memory. Issuing the same
+// number of loads on every path keeps the compiler's wait counts exact: with
+// loads skipped by a branch, it must assume the fewest loads in flight and
+// waits for the whole prefetch at every step.
+constexpr int kTileBytes = kTileElems * 2;
+constexpr int kBufferWord3 = 0x00020000;  // gfx9 buffer resource, dword 3
+constexpr int kNontemporal = 2;           // cache policy bit: streaming access
+
+__device__ inline int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base, bool valid) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* u = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, uniform(valid) ? kTileBytes : 0,
+                                           kBufferWord3);
+}
+__device__ inline u32x4_t tile_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(u32x4_t,
+                            __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kNontemporal));
+}
+__device__ inline s16x4_t tile_load8(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(s16x4_t,
+                            __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, kNontemporal));
+}
+
 // ----------------------------------------------------------------- coherent access
 
 // Partials written by one slice and merged by another (possibly on another
@@ -82,21 +113,18 @@ __device__ inline int partial_slot(int32_t s, int32_t slice_first, int32_t first
 }
 
 // Number of slices for W positions. With min_tiles > 0: W / min_tiles, capped.
-// With min_tiles == 0 (the default policy): whole multiples of `quantum` (one
-// 4-wave workgroup per CU) so every CU gets the same share, stepping up to
-// two workgroups per CU once slices still hold kAutoTilesPerSlice positions;
-// small batches get W / 8 slices.
-constexpr int32_t kAutoTilesPerSlice = 40;
+// With min_tiles == 0 (the default policy): `quantum` slices, one 4-wave
+// workgroup per CU, so every CU gets the same share; small batches get W / 8
+// slices. Measured: two workgroups per CU are never faster (2-3 % slower on
+// long requests: more streams in flight lower the HBM efficiency), and counts
+// that give some CUs two workgroups and others one are 10-25 % slower.
 constexpr int32_t kSmallTilesPerSlice = 8;
 
 __host__ __device__ inline int32_t slice_count(int32_t W, int32_t min_tiles, int32_t max_slices,
                                                int32_t quantum) {
   if (W <= 0) return 0;
   if (min_tiles > 0) return min(max(W / min_tiles, 1), max_slices);
-  int32_t n;
-  if (W >= 2 * quantum * kAutoTilesPerSlice) n = 2 * quantum;
-  else if (W >= quantum * kSmallTilesPerSlice) n = quantum;
-  else n = max(W / kSmallTilesPerSlice, 1);
+  const int32_t n = W >= quantum * kSmallTilesPerSlice ? quantum : max(W / kSmallTilesPerSlice, 1);
   return min(n, max_slices);
 }
 
@@ -104,9 +132,25 @@ struct SliceInfo {
   int32_t W, n;      // total positions, slices
   int32_t s0, s1;    // this slice's position range
   int32_t b, g, x;   // pair holding position s0 and the offset of s0 inside it
+  int32_t L;         // clamped length of request b, or -1 when the plan does not hold it
 };
 
 // ----------------------------------------------------------------- wave helpers
+
+// The plan is the same in every lane; saying so lets the compiler keep the
+// slice walk in scalar registers (tile addresses must be scalar for buffer
+// resources).
+__device__ inline SliceInfo make_uniform(SliceInfo si) {
+  si.W = uniform(si.W);
+  si.n = uniform(si.n);
+  si.s0 = uniform(si.s0);
+  si.s1 = uniform(si.s1);
+  si.b = uniform(si.b);
+  si.g = uniform(si.g);
+  si.x = uniform(si.x);
+  si.L = uniform(si.L);
+  return si;
+}
 
 __device__ inline int32_t wave_sum_i32(int32_t v) {
 #pragma unroll
@@ -146,7 +190,8 @@ __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
   si.b = a.b;
   si.g = a.g;
   si.x = a.x;
-  return si;
+  si.L = -1;
+  return make_uniform(si);
 }
 
 // Slice computed by the wavefront itself from seq_lens (fused launch): a
@@ -155,11 +200,18 @@ __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
 // lane group, up to kPlanRegs groups per load round.
 constexpr int kPlanRegs = 16;
 
-// Weights of requests base + 64r + lane, r < kPlanRegs (0 past the batch).
-// Loads use a clamped index so that all of them issue before any is waited on.
+// s_waitcnt immediate (gfx9 encoding) that waits for vmcnt == 0 and leaves the
+// export and LDS/scalar counters alone.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Tiles before the end of a segment at which the fast-merge counter is read.
+constexpr int32_t kMergeCheckAhead = 3;
+
+// Weights of requests base + 64r + lane, r < kPlanRegs (0 past the batch), and
+// their raw lengths. Loads use a clamped index so that all of them issue before
+// any is waited on.
 __device__ inline void load_weights(const DecodeParams& p, int base, int lane,
-                                    int32_t (&w)[kPlanRegs]) {
-  int32_t raw[kPlanRegs];
+                                    int32_t (&w)[kPlanRegs], int32_t (&raw)[kPlanRegs]) {
 #pragma unroll
   for (int r = 0; r < kPlanRegs; ++r) raw[r] = p.lens[min(base + r * kWave + lane, p.batch - 1)];
 #pragma unroll
@@ -170,16 +222,16 @@ __device__ inline void load_weights(const DecodeParams& p, int base, int lane,
 __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int lane) {
   SliceInfo si;
   constexpr int kChunk = kWave * kPlanRegs;
-  int32_t w[kPlanRegs];
+  int32_t w[kPlanRegs], raw[kPlanRegs];
   int32_t total = 0;
   for (int base = 0; base < p.batch; base += kChunk) {
-    load_weights(p, base, lane, w);
+    load_weights(p, base, lane, w, raw);
     int32_t s = 0;
 #pragma unroll
     for (int r = 0; r < kPlanRegs; ++r) s += w[r];
     total += wave_sum_i32(s);
   }
-  si.W = total * p.hkv;
+  si.W = uniform(total * p.hkv);
   si.n = slice_count(si.W, p.min_tiles, p.max_slices, p.slice_quantum);
   if (wave >= si.n) return si;
   si.s0 = slice_start(wave, si.W, si.n);
@@ -188,9 +240,9 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   // Request b holds positions [hkv*P_b, hkv*P_{b+1}) with P the weight prefix sum.
   const int32_t u = si.s0 / p.hkv;
   int32_t carry = 0;
-  int32_t found_b = -1, found_p = 0;
+  int32_t found_b = -1, found_p = 0, found_w = 1, found_len = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
-    if (p.batch > kChunk) load_weights(p, base, lane, w);
+    if (p.batch > kChunk) load_weights(p, base, lane, w, raw);
 #pragma unroll
     for (int r = 0; r < kPlanRegs; ++r) {
       if (found_b >= 0) break;
@@ -201,25 +253,32 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
         const int first = __ffsll((unsigned long long)hit) - 1;
         found_b = base + r * kWave + first;
         found_p = carry + __shfl(incl - w[r], first);
+        found_w = __shfl(w[r], first);
+        found_len = __shfl(raw[r], first);
       } else {
         carry += cs;
       }
     }
   }
-  const int32_t wb = pair_weight(p.lens[found_b], p.mbps);
+  // The request's weight and length come from the registers already loaded:
+  // no second round trip to seq_lens before the first table row.
   const int32_t rem = si.s0 - p.hkv * found_p;
   si.b = found_b;
-  si.g = rem / wb;
-  si.x = rem % wb;
-  return si;
+  si.g = rem / found_w;
+  si.x = rem % found_w;
+  si.L = clamp_len(found_len, p.mbps);
+  return make_uniform(si);
 }
 
 // ----------------------------------------------------------------- outputs
 
 // Requests with no tokens get a zero row; every wavefront takes a strided share.
-__device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwaves, int lane) {
+// len0: seq_lens[wave] (any value when wave >= batch), loaded by the caller
+// before the plan so that its round trip overlaps the plan's.
+__device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwaves, int lane,
+                                       int32_t len0) {
   for (int b = wave; b < p.batch; b += nwaves) {
-    if (clamp_len(p.lens[b], p.mbps) != 0) continue;
+    if (clamp_len(b == wave ? len0 : p.lens[b], p.mbps) != 0) continue;
     f32x4_t* row = reinterpret_cast<f32x4_t*>(p.out + (size_t)b * p.hq * kHeadDim);
     const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
     for (int i = lane; i < p.hq * (kHeadDim / 4); i += kWave) row[i] = z;
@@ -387,8 +446,9 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   const int wv = threadIdx.x >> 6;
   const int wave = blockIdx.x * kWavesPerGroup + wv;
   const int nwaves = gridDim.x * kWavesPerGroup;
-  zero_empty_rows(p, wave, nwaves, lane);
+  const int32_t len0 = wave < p.batch ? p.lens[wave] : 0;
   const SliceInfo si = kSched == kStaged ? read_plan(p, wave) : plan_in_wave(p, wave, lane);
+  zero_empty_rows(p, wave, nwaves, lane, len0);
   if (kSched == kTwoKernel && lane == 0) {
     // Record the plan for the combine kernel.
     if (wave < si.n) {
@@ -434,11 +494,11 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   int32_t pos = si.s0;  // weighted position reached
   int b = si.b, g = si.g;
   int32_t x = si.x;     // offset of pos inside pair (b, g)
-  // Prefetched for the next pair while the current one streams: its
-  // request's length and first 64 block ids (request pf_b), so that a new
-  // pair's q and first tiles go out together instead of after two dependent
-  // round trips (length, then table row).
-  int32_t pf_b = -1, pf_L = 0, pf_vals = 0;
+  // Known ahead of use: the length of request pf_b (from the plan for the
+  // first pair, prefetched for later ones) and the first 64 block ids of
+  // request pf_tb (prefetched while the previous pair streams), so that a new
+  // pair's q and first tiles go out without dependent round trips.
+  int32_t pf_b = si.L >= 0 ? si.b : -1, pf_L = si.L, pf_tb = -1, pf_vals = 0;
   while (b < p.batch) {
     const int32_t L = pf_b == b ? pf_L : clamp_len(p.lens[b], p.mbps);
     const int32_t nb = (L + kBlock - 1) / kBlock;
@@ -457,7 +517,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // Block ids of this row, 64 at a time, one per lane.
     const int32_t* trow = p.table + (size_t)b * p.mbps;
     int32_t tbase = j;
-    int32_t tvals = (j == 0 && pf_b == b) ? pf_vals : ((tbase + lane < jend) ? trow[tbase + lane] : 0);
+    int32_t tvals = (j == 0 && pf_tb == b) ? pf_vals : ((tbase + lane < jend) ? trow[tbase + lane] : 0);
     // The next pair is (b, g+1) or (b+1, 0); the next request's length is
     // requested now and used after this pair's first tile loads are out.
     const int32_t nq = g + 1 < p.hkv ? b : b + 1;
@@ -466,6 +526,10 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       if (jj - tbase >= kWave) {
         tbase += kWave;
         tvals = (tbase + lane < jend) ? trow[tbase + lane] : 0;
+        // Wait for the new ids here, on the refresh path only. Without this
+        // explicit wait the compiler puts a full vmcnt(0) after the branch
+        // joins, on every tile, and that drains the tile prefetch each step.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       }
       const int32_t id = __builtin_amdgcn_readlane(tvals, jj - tbase);
       return (size_t)min((uint32_t)id, (uint32_t)(p.num_blocks - 1)) * blk_stride +
@@ -477,13 +541,14 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     typename F::State st;
     F::init(st);
 
+    // Every step issues one tile's loads; tiles past jend are empty (their
+    // index is clamped to a real tile, their resource has size 0).
     typename F::Tile buf[PF + 1];
 #pragma unroll
-    for (int i = 0; i < PF; ++i)
-      if (j + i < jend) {
-        const size_t off = tile_off(j + i);
-        F::load_tile(buf[i], p.k + off, p.v + off, lane);
-      }
+    for (int i = 0; i < PF; ++i) {
+      const size_t off = tile_off(min(j + i, jend - 1));
+      F::load_tile(buf[i], p.k + off, p.v + off, j + i < jend, lane);
+    }
 
     // Prefetch for the next pair (in bounds: lanes below its block count,
     // which is at most the table's row length).
@@ -492,7 +557,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       const int32_t nbq = (Lq + kBlock - 1) / kBlock;
       const int32_t* tq = p.table + (size_t)nq * p.mbps;
       pf_vals = lane < min(nbq, kWave) ? tq[lane] : 0;
-      pf_b = nq;
+      pf_b = pf_tb = nq;
       pf_L = Lq;
     }
 
@@ -500,29 +565,31 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // (the next one), which handles its share of the pair first: if it has
     // already arrived, this slice will be the last, so it merges straight
     // from registers after its tiles (no partial of its own, no atomic, one
-    // round trip for the other partial). The counter is read here, after
-    // the first tile loads are out, and only looked at after the tiles.
-    bool merge_now = false;
-    if constexpr (kMergeHere && F::kFastMerge) {
-      if (j == 0 && jend < nb && slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1) {
-        const int32_t seen = __hip_atomic_load(p.counters + wave, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-        merge_now = __builtin_amdgcn_readfirstlane(seen) == 1;
-      }
-    }
+    // round trip for the other partial). The counter is read a few tiles
+    // before the segment ends (late enough that the next slice has usually
+    // finished its share, early enough that the read's latency hides behind
+    // the remaining tiles) and only looked at after the tiles.
+    bool fast_cand = false;
+    if constexpr (kMergeHere && F::kFastMerge)
+      fast_cand = j == 0 && jend < nb && slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1;
+    const int32_t check_at = fast_cand ? max(j, jend - kMergeCheckAhead) : -1;
+    int32_t seen = 0;
     for (int32_t jj = j; jj < jend; jj += PF + 1) {
 #pragma unroll
       for (int u = 0; u <= PF; ++u) {
         const int32_t cur = jj + u;
         if (cur >= jend) break;
         const int32_t ld = cur + PF;
-        if (ld < jend) {
-          const size_t off = tile_off(ld);
-          F::load_tile(buf[(u + PF) % (PF + 1)], p.k + off, p.v + off, lane);
+        {
+          const size_t off = tile_off(min(ld, jend - 1));
+          F::load_tile(buf[(u + PF) % (PF + 1)], p.k + off, p.v + off, ld < jend, lane);
         }
+        if (cur == check_at)
+          seen = __hip_atomic_load(p.counters + wave, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         F::step(st, buf[u], qr, L - cur * kBlock, p.scale_log2, lane, sh);
       }
     }
+    const bool merge_now = fast_cand && __builtin_amdgcn_readfirstlane(seen) == 1;
 
     if (j == 0 && jend == nb) {
       F::template write<false>(st, p.out + ((size_t)b * p.hq + g * G) * kHeadDim, nullptr, lane);

@@ -62,19 +62,20 @@ struct MfmaFamily {
     st.l = 0.f;
   }
 
-  __device__ static void load_tile(Tile& x, const uint16_t* __restrict__ kbase,
-                                   const uint16_t* __restrict__ vbase, int lane) {
+  // valid == false: the tile is past the segment; its registers read zeros
+  // and no memory is touched.
+  __device__ static void load_tile(Tile& x, const uint16_t* kbase, const uint16_t* vbase,
+                                   bool valid, int lane) {
     const int col = lane & 15, rq = lane >> 4;
     // Each KV tile is read exactly once: nontemporal loads keep it from
     // displacing reusable lines in the caches.
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, valid), rv = tile_rsrc(vbase, valid);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
-      x.k[kb] = __builtin_nontemporal_load(
-          reinterpret_cast<const bf16x8_t*>(kbase + kPiece * (kWave * kb + lane)));
+      x.k[kb] = __builtin_bit_cast(bf16x8_t, tile_load16(rk, 2 * kPiece * (kWave * kb + lane)));
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb)
-      x.v[mb] = __builtin_nontemporal_load(
-          reinterpret_cast<const s16x4_t*>(vbase + (16 * mb + col) * kBlock + 4 * rq));
+      x.v[mb] = tile_load8(rv, 2 * ((16 * mb + col) * kBlock + 4 * rq));
   }
 
   __device__ static void step(State& st, Tile& x, const Q& q, int32_t valid, float scale_log2,
@@ -197,7 +198,10 @@ struct MfmaFamily {
 
 template <int G, Schedule kSched>
 __global__ __launch_bounds__(kWave * kWavesPerGroup, 2) void decode_mfma_kernel(DecodeParams p) {
-  decode_driver<MfmaFamily<G>, G, 2, kSched>(p);
+  // One tile in flight ahead of the one being computed: with 4 waves on every
+  // CU that keeps HBM saturated; deeper prefetch measured equal or slower
+  // (more requests in flight lower the HBM efficiency).
+  decode_driver<MfmaFamily<G>, G, 1, kSched>(p);
 }
 
 template <int G>

@@ -86,17 +86,16 @@ struct ValuFamily {
     }
   }
 
-  __device__ static void load_tile(Tile& x, const uint16_t* __restrict__ kbase,
-                                   const uint16_t* __restrict__ vbase, int lane) {
+  // valid == false: the tile is past the segment; its registers read zeros
+  // and no memory is touched.
+  __device__ static void load_tile(Tile& x, const uint16_t* kbase, const uint16_t* vbase,
+                                   bool valid, int lane) {
     const int r = lane >> 4, c = lane & 15;
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, valid), rv = tile_rsrc(vbase, valid);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      x.k[i] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4_t*>(kbase + (c * kBlock + 4 * i + r) * kPiece));
+    for (int i = 0; i < 4; ++i) x.k[i] = tile_load16(rk, 2 * (c * kBlock + 4 * i + r) * kPiece);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      x.v[i] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4_t*>(vbase + 512 * i + 8 * lane));
+    for (int i = 0; i < 4; ++i) x.v[i] = tile_load16(rv, 2 * (512 * i + 8 * lane));
   }
 
   __device__ static void step(State& st, Tile& x, const Q& q, int32_t valid, float scale_log2,
