@@ -114,11 +114,13 @@ __device__ inline int partial_slot(int32_t s, int32_t slice_first, int32_t first
 
 // Number of slices for W positions. With min_tiles > 0: W / min_tiles, capped.
 // With min_tiles == 0 (the default policy): `quantum` slices, one 4-wave
-// workgroup per CU, so every CU gets the same share; small batches get W / 8
-// slices. Measured: two workgroups per CU are never faster (2-3 % slower on
-// long requests: more streams in flight lower the HBM efficiency), and counts
-// that give some CUs two workgroups and others one are 10-25 % slower.
-constexpr int32_t kSmallTilesPerSlice = 8;
+// workgroup per CU, so every CU gets the same share; batches too small for
+// that get W / 2 slices. Measured: two workgroups per CU are never faster
+// (2-3 % slower on long requests: more streams in flight lower the HBM
+// efficiency), counts that give some CUs two workgroups and others one are
+// 10-25 % slower, and a small batch (4 requests of 64-512 tokens) is fastest
+// with the most slices up to one workgroup per CU (W / 8 slices: 13 % slower).
+constexpr int32_t kSmallTilesPerSlice = 2;
 
 __host__ __device__ inline int32_t slice_count(int32_t W, int32_t min_tiles, int32_t max_slices,
                                                int32_t quantum) {
