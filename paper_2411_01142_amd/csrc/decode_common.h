@@ -206,6 +206,10 @@ constexpr int kPlanRegs = 16;
 // export and LDS/scalar counters alone.
 constexpr int kWaitVmcnt0 = 0x0F70;
 
+// Slices of at least this many positions on average merge within a workgroup
+// through LDS (fused launch).
+constexpr int32_t kGroupMergeMinTiles = 8;
+
 // Tiles before the end of a segment at which the fast-merge counter is read.
 constexpr int32_t kMergeCheckAhead = 3;
 
@@ -290,20 +294,20 @@ __device__ inline void zero_empty_rows(const DecodeParams& p, int wave, int nwav
 // out rows of pair (b, g) from two contributors' log-sum-exps and rows (this
 // lane's two dims): the two-contributor case of merge_pair, operation for
 // operation.
-template <int G>
+template <int G, int GH = G>
 __device__ inline void merge_two_values(const DecodeParams& p, int32_t b, int32_t g,
                                         const float* la, const float* lb, const float2* oa,
-                                        const float2* ob, int lane) {
+                                        const float2* ob, int lane, int h0 = 0) {
   const int d = 2 * lane;
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
+  for (int h = 0; h < GH; ++h) {
     const float m = fmaxf(la[h], lb[h]);
     const float wa = __expf(la[h] - m), wb = __expf(lb[h] - m);
     const float inv = 1.f / (wa + wb);
     float2 r;
     r.x = fmaf(wb, ob[h].x, wa * oa[h].x) * inv;
     r.y = fmaf(wb, ob[h].y, wa * oa[h].y) * inv;
-    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
+    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h0 + h) * kHeadDim + d) = r;
   }
 }
 
@@ -313,36 +317,42 @@ __device__ inline void merge_two_values(const DecodeParams& p, int32_t b, int32_
 // (earlier sums are rescaled when it grows). Lane i reads the log-sum-exps of
 // contributor i of the chunk; each lane owns dims 2*lane, 2*lane+1 of the
 // sums; partial rows are read kBatch contributors at a time, the first batch
-// issued together with the log-sum-exps. kCoherent: the partials were written
-// by other wavefronts of the running kernel.
-template <int G, bool kCoherent>
-__device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, int32_t first_tile,
-                                  int32_t c0, int32_t c1, int32_t W, int32_t n, int lane) {
-  constexpr int kBatch = 32 / G > 16 ? 16 : (32 / G > 0 ? 32 / G : 1);  // 64 registers
+// issued together with the log-sum-exps. Partial slot q lives at
+// part_o[(q - slot0) * G * 128], part_lse[(q - slot0) * G] (the workspace, or a
+// workgroup's shared copy). kCoherent: the partials were written by other
+// wavefronts of the running kernel to the workspace. kMaxBatch caps the rows
+// read per round (LDS reads need no batching; the sums are the same either way).
+template <int G, int GH, bool kCoherent, int kMaxBatch>
+__device__ inline void merge_pair_heads(const DecodeParams& p, const float* part_o,
+                                        const float* part_lse, int32_t slot0, int32_t b,
+                                        int32_t g, int h0, int32_t first_tile, int32_t c0,
+                                        int32_t c1, int32_t W, int32_t n, int lane) {
+  constexpr int kFit = 32 / GH > 0 ? 32 / GH : 1;  // 64 registers of rows
+  constexpr int kBatch = kFit < kMaxBatch ? kFit : kMaxBatch;
   auto ld = [](const float* a) -> float { return kCoherent ? load_coherent(a) : *a; };
   auto ld2 = [](const float* a) -> float2 {
     return kCoherent ? load_coherent2(a) : *reinterpret_cast<const float2*>(a);
   };
   const int k = c1 - c0 + 1;
   const int d = 2 * lane;
-  float m[G], z[G], a0[G], a1[G];
+  float m[GH], z[GH], a0[GH], a1[GH];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
+  for (int h = 0; h < GH; ++h) {
     m[h] = -INFINITY;
     z[h] = a0[h] = a1[h] = 0.f;
   }
   for (int base = 0; base < k; base += kWave) {
     const int cnt = min(kWave, k - base);
-    float ov[kBatch][G][2];
+    float ov[kBatch][GH][2];
     auto load_rows = [&](int i0, bool clamp) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         if (!clamp && i0 + u >= cnt) break;  // uniform
         const int c = c0 + base + min(i0 + u, cnt - 1);
-        const int slot = partial_slot(c, slice_start(c, W, n), first_tile);
+        const int slot = partial_slot(c, slice_start(c, W, n), first_tile) - slot0;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float2 v = ld2(p.part_o + ((size_t)slot * G + h) * kHeadDim + d);
+        for (int h = 0; h < GH; ++h) {
+          const float2 v = ld2(part_o + ((size_t)slot * G + h0 + h) * kHeadDim + d);
           ov[u][h][0] = v.x;
           ov[u][h][1] = v.y;
         }
@@ -350,15 +360,15 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
     };
     load_rows(0, true);
     const int mine = c0 + base + (lane < cnt ? lane : 0);
-    const int my_slot = partial_slot(mine, slice_start(mine, W, n), first_tile);
+    const int my_slot = partial_slot(mine, slice_start(mine, W, n), first_tile) - slot0;
     // Every head's log-sum-exp is loaded before any cross-lane step, so the
     // loads share one round trip.
-    float lse_h[G];
+    float lse_h[GH];
 #pragma unroll
-    for (int h = 0; h < G; ++h) lse_h[h] = ld(p.part_lse + my_slot * G + h);
-    float w[G];
+    for (int h = 0; h < GH; ++h) lse_h[h] = ld(part_lse + my_slot * G + h0 + h);
+    float w[GH];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
+    for (int h = 0; h < GH; ++h) {
       const float lse = lane < cnt ? lse_h[h] : -INFINITY;
       const float mc = fmaxf(m[h], wave_max_f32(lse));
       const float rescale = __expf(m[h] - mc);  // 0 on the first chunk
@@ -375,7 +385,7 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
       for (int u = 0; u < kBatch; ++u) {
         if (i0 + u >= cnt) break;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+        for (int h = 0; h < GH; ++h) {
           const float wi = __shfl(w[h], i0 + u);
           a0[h] = fmaf(wi, ov[u][h][0], a0[h]);
           a1[h] = fmaf(wi, ov[u][h][1], a1[h]);
@@ -384,42 +394,58 @@ __device__ inline void merge_pair(const DecodeParams& p, int32_t b, int32_t g, i
     }
   }
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
+  for (int h = 0; h < GH; ++h) {
     const float inv = 1.f / z[h];
     float2 r;
     r.x = a0[h] * inv;
     r.y = a1[h] * inv;
-    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h) * kHeadDim + d) = r;
+    *reinterpret_cast<float2*>(p.out + ((size_t)b * p.hq + g * G + h0 + h) * kHeadDim + d) = r;
   }
 }
 
+// All heads of the pair, GH of them per pass (fewer live registers).
+template <int G, bool kCoherent, int kMaxBatch = 16, int GH = G>
+__device__ inline void merge_pair(const DecodeParams& p, const float* part_o,
+                                  const float* part_lse, int32_t slot0, int32_t b, int32_t g,
+                                  int32_t first_tile, int32_t c0, int32_t c1, int32_t W,
+                                  int32_t n, int lane) {
+  static_assert(G % GH == 0, "head passes must tile the group");
+  for (int h0 = 0; h0 < G; h0 += GH)
+    merge_pair_heads<G, GH, kCoherent, kMaxBatch>(p, part_o, part_lse, slot0, b, g, h0,
+                                                  first_tile, c0, c1, W, n, lane);
+}
+
 // The merge of a pair with exactly two contributors, partial slots sa (the
-// earlier slice) and sb, with every load in one round trip. Same arithmetic,
-// in the same order, as merge_pair for two contributors, so both give the
-// same bits.
-template <int G, bool kCoherent>
-__device__ inline void merge_two(const DecodeParams& p, int32_t b, int32_t g, int32_t sa,
+// earlier slice) and sb of part_o / part_lse, with every load in one round
+// trip. Same arithmetic, in the same order, as merge_pair for two
+// contributors, so both give the same bits.
+template <int G, bool kCoherent, int GH = G>
+__device__ inline void merge_two(const DecodeParams& p, const float* part_o,
+                                 const float* part_lse, int32_t b, int32_t g, int32_t sa,
                                  int32_t sb, int lane) {
+  static_assert(G % GH == 0, "head passes must tile the group");
   const int d = 2 * lane;
-  float la[G], lb[G];
-  float2 oa[G], ob[G];
+  for (int h0 = 0; h0 < G; h0 += GH) {
+    float la[GH], lb[GH];
+    float2 oa[GH], ob[GH];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float* pa = p.part_o + ((size_t)sa * G + h) * kHeadDim + d;
-    const float* pb = p.part_o + ((size_t)sb * G + h) * kHeadDim + d;
-    if (kCoherent) {
-      la[h] = load_coherent(p.part_lse + sa * G + h);
-      lb[h] = load_coherent(p.part_lse + sb * G + h);
-      oa[h] = load_coherent2(pa);
-      ob[h] = load_coherent2(pb);
-    } else {
-      la[h] = p.part_lse[sa * G + h];
-      lb[h] = p.part_lse[sb * G + h];
-      oa[h] = *reinterpret_cast<const float2*>(pa);
-      ob[h] = *reinterpret_cast<const float2*>(pb);
+    for (int h = 0; h < GH; ++h) {
+      const float* pa = part_o + ((size_t)sa * G + h0 + h) * kHeadDim + d;
+      const float* pb = part_o + ((size_t)sb * G + h0 + h) * kHeadDim + d;
+      if (kCoherent) {
+        la[h] = load_coherent(part_lse + sa * G + h0 + h);
+        lb[h] = load_coherent(part_lse + sb * G + h0 + h);
+        oa[h] = load_coherent2(pa);
+        ob[h] = load_coherent2(pb);
+      } else {
+        la[h] = part_lse[sa * G + h0 + h];
+        lb[h] = part_lse[sb * G + h0 + h];
+        oa[h] = *reinterpret_cast<const float2*>(pa);
+        ob[h] = *reinterpret_cast<const float2*>(pb);
+      }
     }
+    merge_two_values<G, GH>(p, b, g, la, lb, oa, ob, lane, h0);
   }
-  merge_two_values<G>(p, b, g, la, lb, oa, ob, lane);
 }
 
 // Fused launch: after writing its partial for a cut pair, a slice counts itself
@@ -439,6 +465,31 @@ __device__ inline bool arrive_last(const DecodeParams& p, int32_t c0, int32_t c1
 
 // ----------------------------------------------------------------- the driver
 
+// Cut pairs whose contributors are all slices of one workgroup (the four
+// waves hold consecutive slices) are merged through LDS: partials, a counter
+// per pair (indexed by its first slice), and the last arrival merges. No
+// device-coherent store has to complete and no atomic crosses the chip, which
+// under load takes several microseconds per cut segment. Pairs that cross a
+// workgroup boundary use the workspace.
+template <int G>
+struct GroupMerge {
+  static constexpr int kHeadsPerPass = G < 4 ? G : 4;  // merges from LDS: 4 heads at a time
+  float o[2 * kWavesPerGroup][G * kHeadDim];  // partial slot 2s / 2s+1 of slice s, local
+  float lse[2 * kWavesPerGroup][G];
+  int32_t count[kWavesPerGroup];
+};
+// Launches that merge in a separate kernel keep no shared merge state.
+template <int G, bool kOn>
+struct GroupMergeOf {
+  using type = GroupMerge<G>;
+};
+template <int G>
+struct GroupMergeOf<G, false> {
+  struct type {
+    int32_t count[1];
+  };
+};
+
 // Family provides: Tile, State, Q, Shared; load_q, init, load_tile, step, write.
 // PF tiles are in flight ahead of the one being computed.
 template <class F, int G, int PF, Schedule kSched>
@@ -449,8 +500,22 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   const int wave = blockIdx.x * kWavesPerGroup + wv;
   const int nwaves = gridDim.x * kWavesPerGroup;
   const int32_t len0 = wave < p.batch ? p.lens[wave] : 0;
+  // Slices of this workgroup: first_slice .. first_slice + kWavesPerGroup - 1.
+  const int32_t first_slice = blockIdx.x * kWavesPerGroup;
+  __shared__ typename GroupMergeOf<G, kMergeHere>::type gm;
   const SliceInfo si = kSched == kStaged ? read_plan(p, wave) : plan_in_wave(p, wave, lane);
   zero_empty_rows(p, wave, nwaves, lane, len0);
+  // Merges through LDS pay when slices are long enough to hold cut segments
+  // of several tiles; for tiny slices the barrier that clears the counters
+  // costs more than it saves. The plan is the same in every wave of the block,
+  // so all of them take (or skip) the barrier, before any returns.
+  const bool group_merge = kMergeHere && si.n > 0 && si.W >= kGroupMergeMinTiles * si.n;
+  if constexpr (kMergeHere) {
+    if (group_merge) {
+      if (threadIdx.x < kWavesPerGroup) gm.count[threadIdx.x] = 0;
+      __syncthreads();
+    }
+  }
   if (kSched == kTwoKernel && lane == 0) {
     // Record the plan for the combine kernel.
     if (wave < si.n) {
@@ -573,7 +638,9 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // the remaining tiles) and only looked at after the tiles.
     bool fast_cand = false;
     if constexpr (kMergeHere && F::kFastMerge)
-      fast_cand = j == 0 && jend < nb && slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1;
+      fast_cand = j == 0 && jend < nb &&
+                  (!group_merge || wave + 1 == first_slice + kWavesPerGroup) &&
+                  slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1;
     const int32_t check_at = fast_cand ? max(j, jend - kMergeCheckAhead) : -1;
     int32_t seen = 0;
     for (int32_t jj = j; jj < jend; jj += PF + 1) {
@@ -604,6 +671,32 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         F::merge_write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
                        p.out + ((size_t)b * p.hq + g * G) * kHeadDim, lane);
       }
+    } else if (group_merge && slice_of(first_tile, si.W, si.n) >= first_slice &&
+               slice_of(first_tile + nb - 1, si.W, si.n) < first_slice + kWavesPerGroup) {
+      if constexpr (kMergeHere) {
+        // Every contributor is a wave of this workgroup: merge through LDS.
+        const int32_t c0 = slice_of(first_tile, si.W, si.n);
+        const int32_t c1 = slice_of(first_tile + nb - 1, si.W, si.n);
+        const int32_t slot0 = 2 * first_slice;
+        constexpr int kLdsMergeHeads = GroupMerge<G>::kHeadsPerPass;
+        const int ls = partial_slot(wave, si.s0, first_tile) - slot0;
+        F::template write<false>(st, gm.o[ls], gm.lse[ls], lane);
+        int32_t old = 0;
+        if (lane == 0)
+          old = __hip_atomic_fetch_add(&gm.count[c0 - first_slice], 1, __ATOMIC_ACQ_REL,
+                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (__builtin_amdgcn_readlane(old, 0) == c1 - c0) {
+          if (c1 == c0 + 1) {
+            merge_two<G, false, kLdsMergeHeads>(p, &gm.o[0][0], &gm.lse[0][0], b, g,
+                                partial_slot(c0, slice_start(c0, si.W, si.n), first_tile) - slot0,
+                                partial_slot(c1, slice_start(c1, si.W, si.n), first_tile) - slot0,
+                                lane);
+          } else {
+            merge_pair<G, false, 1, kLdsMergeHeads>(p, &gm.o[0][0], &gm.lse[0][0], slot0, b, g,
+                                                    first_tile, c0, c1, si.W, si.n, lane);
+          }
+        }
+      }
     } else {
       const int slot = partial_slot(wave, si.s0, first_tile);
       F::template write<kMergeHere>(st, p.part_o + (size_t)slot * G * kHeadDim,
@@ -631,11 +724,12 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     for (int i = 0; i < npend; ++i) {
       const Pending q = i == 0 ? pend0 : pend1;
       if (q.c1 == q.c0 + 1) {
-        merge_two<G, true>(p, q.b, q.g,
+        merge_two<G, true>(p, p.part_o, p.part_lse, q.b, q.g,
                            partial_slot(q.c0, slice_start(q.c0, si.W, si.n), q.first),
                            partial_slot(q.c1, slice_start(q.c1, si.W, si.n), q.first), lane);
       } else {
-        merge_pair<G, true>(p, q.b, q.g, q.first, q.c0, q.c1, si.W, si.n, lane);
+        merge_pair<G, true>(p, p.part_o, p.part_lse, 0, q.b, q.g, q.first, q.c0, q.c1, si.W,
+                            si.n, lane);
       }
     }
   }

@@ -138,7 +138,7 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeP
     merge_two_values<G>(p, a.b, a.g, la, lb, oa, ob, lane);  // slots 2s-1, 2s
     return;
   }
-  merge_pair<G, false>(p, a.b, a.g, first_tile, s - 1, c1, W, n, lane);
+  merge_pair<G, false>(p, p.part_o, p.part_lse, 0, a.b, a.g, first_tile, s - 1, c1, W, n, lane);
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* __restrict__ dst, size_t words) {

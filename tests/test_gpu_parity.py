@@ -286,6 +286,23 @@ def test_schedules_agree_bit_for_bit():
         assert np.array_equal(a, b) and np.array_equal(a, c)
 
 
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_group_merge_mixes_contributor_counts(variant):
+    # Pairs of 3-190 weighted positions cut by 8-40 slices of >= 8 positions:
+    # cut pairs with 2..7 contributors, some inside one 4-wave workgroup
+    # (merged through LDS), some across workgroups (merged through the
+    # workspace). Fused must match the oracle and, slice for slice, the
+    # two-kernel schedule bit for bit (same merge arithmetic).
+    lens = [800, 40, 1600, 16, 500, 3000, 1, 257]
+    case = W.build_case(lens, 8, 2, 128, 16, seed=31)
+    ref = oracle.decode_attention(case)
+    for slices in (8, 12, 16, 24, 40):
+        a = run(case, variant=variant, schedule="fused", max_slices=slices)
+        b = run(case, variant=variant, schedule="two_kernel", max_slices=slices)
+        assert_parity(a, ref, f"group merge {variant} slices={slices}")
+        assert np.array_equal(a, b), f"fused != two_kernel at {slices} slices"
+
+
 def test_poisoned_slots_do_not_leak():
     lens = [1, 15, 17, 64, 99, 250]
     a = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=True)
