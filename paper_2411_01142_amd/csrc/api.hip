@@ -38,10 +38,7 @@ neo_status clear_error() {
 
 namespace {
 
-template <typename... A>
-neo_status fail(neo_status st, const char* fmt, A... a) {
-  return neo::set_error(st, fmt, a...);
-}
+using neo::set_error;
 
 neo_status ok() { return neo::clear_error(); }
 
@@ -84,7 +81,7 @@ std::atomic<int32_t> g_cu_count[kMaxDevices];
 neo_status device_cu_count(int32_t* cus) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
   if (dev >= 0 && dev < kMaxDevices) {
     const int32_t cached = g_cu_count[dev].load(std::memory_order_relaxed);
     if (cached > 0) {
@@ -95,7 +92,7 @@ neo_status device_cu_count(int32_t* cus) {
   int v = 0;
   e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess || v <= 0)
-    return fail(NEO_ERR_HIP, "hipDeviceGetAttribute(cu count): %s", hipGetErrorString(e));
+    return set_error(NEO_ERR_HIP, "hipDeviceGetAttribute(cu count): %s", hipGetErrorString(e));
   if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(v, std::memory_order_relaxed);
   *cus = v;
   return NEO_OK;
@@ -103,16 +100,17 @@ neo_status device_cu_count(int32_t* cus) {
 
 neo_status check_heads(int32_t hq, int32_t hkv, int32_t head_dim) {
   if (hq <= 0 || hkv <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "num_q_heads (%d) and num_kv_heads (%d) must be positive",
-                hq, hkv);
+    return set_error(NEO_ERR_INVALID_ARG, "num_q_heads (%d) and num_kv_heads (%d) must be positive",
+                     hq, hkv);
   if (hq % hkv != 0)
-    return fail(NEO_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
-                hq, hkv);
+    return set_error(NEO_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                     hq, hkv);
   if (head_dim != neo::kHeadDim)
-    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", head_dim,
-                neo::kHeadDim);
+    return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", head_dim,
+                     neo::kHeadDim);
   if (!supported_group(hq / hkv))
-    return fail(NEO_ERR_UNSUPPORTED, "query group %d unsupported (1, 2, 4, 8 or 16)", hq / hkv);
+    return set_error(NEO_ERR_UNSUPPORTED, "query group %d unsupported (1, 2, 4, 8 or 16)",
+                     hq / hkv);
   return NEO_OK;
 }
 
@@ -126,8 +124,8 @@ const char* neo_version(void) { return "0.1.0"; }
 
 neo_status neo_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                       int32_t head_dim, size_t* bytes_out) {
-  if (!bytes_out) return fail(NEO_ERR_INVALID_ARG, "bytes_out is NULL");
-  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (!bytes_out) return set_error(NEO_ERR_INVALID_ARG, "bytes_out is NULL");
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
   if (st != NEO_OK) return st;
   *bytes_out = neo::workspace_layout(batch, num_q_heads / num_kv_heads).total;
@@ -144,43 +142,44 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        int32_t schedule, int32_t max_slices,
                                        void* decode_start_event, void* decode_end_event,
                                        void* stream) {
-  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
   if (st != NEO_OK) return st;
   if (block_size != neo::kBlock)
-    return fail(NEO_ERR_UNSUPPORTED, "block_size %d unsupported (only %d)", block_size,
-                neo::kBlock);
-  if (!isfinite(scale)) return fail(NEO_ERR_INVALID_ARG, "scale is not finite");
+    return set_error(NEO_ERR_UNSUPPORTED, "block_size %d unsupported (only %d)", block_size,
+                     neo::kBlock);
+  if (!isfinite(scale)) return set_error(NEO_ERR_INVALID_ARG, "scale is not finite");
   if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
-    return fail(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
+    return set_error(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
   if (schedule != NEO_SCHEDULE_AUTO && schedule != NEO_SCHEDULE_FUSED &&
       schedule != NEO_SCHEDULE_STAGED && schedule != NEO_SCHEDULE_TWO_KERNEL)
-    return fail(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
+    return set_error(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
   if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
-    return fail(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
-                NEO_MAX_SLICES);
+    return set_error(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
+                     NEO_MAX_SLICES);
   if (batch == 0) return ok();
   if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
-    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
-                max_blocks_per_seq, num_blocks);
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
+                     max_blocks_per_seq, num_blocks);
   if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCost) * num_kv_heads >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG,
-                "batch * (max_blocks_per_seq + 2) * num_kv_heads must stay below 2^31");
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "batch * (max_blocks_per_seq + 2) * num_kv_heads must stay below 2^31");
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
-    return fail(NEO_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
   if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
-    return fail(NEO_ERR_INVALID_ARG, "block_table and seq_lens must be 4-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "block_table and seq_lens must be 4-byte aligned");
   const int32_t group = num_q_heads / num_kv_heads;
   const neo::WorkspaceLayout wl = neo::workspace_layout(batch, group);
   if (!workspace || workspace_bytes < wl.total)
-    return fail(NEO_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", wl.total,
-                workspace ? workspace_bytes : (size_t)0);
+    return set_error(NEO_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", wl.total,
+                     workspace ? workspace_bytes : (size_t)0);
   if (!aligned(workspace, 256))
-    return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
   int32_t cus = 0;
   st = device_cu_count(&cus);
@@ -230,23 +229,23 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                          quantum, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
                          reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
                          reinterpret_cast<int32_t*>(ws + wl.prefix), s);
-    if (e != hipSuccess) return fail(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return set_error(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
   }
   const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
   if (decode_start_event) {
     e = hipEventRecord(static_cast<hipEvent_t>(decode_start_event), s);
-    if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return set_error(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
   e = variant == NEO_VARIANT_VALU ? neo::launch_decode_valu(p, group, sched, grid, s)
                                   : neo::launch_decode_mfma(p, group, sched, grid, s);
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   if (decode_end_event) {
     e = hipEventRecord(static_cast<hipEvent_t>(decode_end_event), s);
-    if (e != hipSuccess) return fail(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return set_error(NEO_ERR_HIP, "event record: %s", hipGetErrorString(e));
   }
   if (sched != neo::kFused) {
     e = neo::launch_combine(p, group, grid, s);
-    if (e != hipSuccess) return fail(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return set_error(NEO_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
   }
   return ok();
 }
@@ -278,12 +277,12 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
 }
 
 neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
-  if (!workspace) return fail(NEO_ERR_INVALID_ARG, "workspace is NULL");
+  if (!workspace) return set_error(NEO_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned(workspace, 256))
-    return fail(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   hipError_t e = neo::launch_fill_zero(workspace, workspace_bytes & ~(size_t)3,
                                        static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "fill launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "fill launch: %s", hipGetErrorString(e));
   return ok();
 }
 
@@ -291,24 +290,24 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
                             const int32_t* seq_lens, const int32_t* token_offsets, int32_t batch,
                             int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
                             int32_t block_size, int32_t num_blocks, void* dst, void* stream) {
-  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
-  if (is_v != 0 && is_v != 1) return fail(NEO_ERR_INVALID_ARG, "is_v must be 0 or 1");
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (is_v != 0 && is_v != 1) return set_error(NEO_ERR_INVALID_ARG, "is_v must be 0 or 1");
   if (num_kv_heads <= 0 || head_dim <= 0 || head_dim % neo::kPiece != 0 || block_size <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "bad shape (num_kv_heads %d, head_dim %d, block_size %d)",
-                num_kv_heads, head_dim, block_size);
+    return set_error(NEO_ERR_INVALID_ARG, "bad shape (num_kv_heads %d, head_dim %d, block_size %d)",
+                     num_kv_heads, head_dim, block_size);
   if (batch == 0) return ok();
   if (!cache || !block_table || !seq_lens || !token_offsets || !dst)
-    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
-  if (batch > 65535) return fail(NEO_ERR_INVALID_ARG, "batch above 65535");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  if (batch > 65535) return set_error(NEO_ERR_INVALID_ARG, "batch above 65535");
   if ((int64_t)max_blocks_per_seq * block_size >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   hipError_t e = neo::launch_gather(static_cast<const uint16_t*>(cache), is_v, block_table,
                                     seq_lens, token_offsets, batch, max_blocks_per_seq,
                                     num_kv_heads, head_dim, block_size, num_blocks,
                                     static_cast<uint16_t*>(dst), static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "gather launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "gather launch: %s", hipGetErrorString(e));
   return ok();
 }
 
@@ -316,28 +315,28 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
                          const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
                          int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
                          int32_t block_size, int32_t num_blocks, void* stream) {
-  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
-  if (num_kv_heads <= 0) return fail(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (num_kv_heads <= 0) return set_error(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
   if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
-    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
-                head_dim, block_size);
+    return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
+                     head_dim, block_size);
   if (batch == 0) return ok();
   if (!k_cache || !v_cache || !k_new || !v_new || !block_table || !seq_lens)
-    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   if ((int64_t)batch * num_kv_heads >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG, "batch * num_kv_heads must be below 2^31");
+    return set_error(NEO_ERR_INVALID_ARG, "batch * num_kv_heads must be below 2^31");
   if (!aligned(k_cache, 16) || !aligned(k_new, 16) || !aligned(v_cache, 2) || !aligned(v_new, 2))
-    return fail(NEO_ERR_INVALID_ARG, "k_cache and k_new must be 16-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "k_cache and k_new must be 16-byte aligned");
   hipError_t e = neo::launch_kv_append(
       static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
       static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), block_table,
       seq_lens, batch, max_blocks_per_seq, num_kv_heads, num_blocks,
       static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "append launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "append launch: %s", hipGetErrorString(e));
   return ok();
 }
 
@@ -345,18 +344,18 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
                               const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
                               int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                               int32_t src_num_blocks, int32_t dst_num_blocks, void* stream) {
-  if (n < 0) return fail(NEO_ERR_INVALID_ARG, "n (%d) is negative", n);
-  if (num_kv_heads <= 0) return fail(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
+  if (n < 0) return set_error(NEO_ERR_INVALID_ARG, "n (%d) is negative", n);
+  if (num_kv_heads <= 0) return set_error(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
   if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
-    return fail(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
-                head_dim, block_size);
+    return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
+                     head_dim, block_size);
   if (n == 0) return ok();
   if (!src_k || !src_v || !dst_k || !dst_v || !src_ids || !dst_ids)
-    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (src_num_blocks <= 0 || dst_num_blocks <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "block counts must be positive");
+    return set_error(NEO_ERR_INVALID_ARG, "block counts must be positive");
   if (!aligned(src_k, 16) || !aligned(src_v, 16) || !aligned(dst_k, 16) || !aligned(dst_v, 16))
-    return fail(NEO_ERR_INVALID_ARG, "caches must be 16-byte aligned");
+    return set_error(NEO_ERR_INVALID_ARG, "caches must be 16-byte aligned");
   // Every pointer the kernel dereferences must be device memory or pinned host
   // memory; pageable host memory would fault the kernel, so it is refused here.
   const void* ptrs[6] = {src_k, src_v, dst_k, dst_v, src_ids, dst_ids};
@@ -365,34 +364,34 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
   for (int i = 0; i < 6; ++i) {
     dev[i] = device_address(ptrs[i]);
     if (!dev[i])
-      return fail(NEO_ERR_INVALID_ARG,
-                  "%s is not device memory or pinned host memory the device can address",
-                  names[i]);
+      return set_error(NEO_ERR_INVALID_ARG,
+                       "%s is not device memory or pinned host memory the device can address",
+                       names[i]);
   }
   hipError_t e = neo::launch_copy_blocks(
       static_cast<const uint16_t*>(dev[0]), static_cast<const uint16_t*>(dev[1]),
       static_cast<uint16_t*>(dev[2]), static_cast<uint16_t*>(dev[3]),
       static_cast<const int32_t*>(dev[4]), static_cast<const int32_t*>(dev[5]), n, num_kv_heads,
       src_num_blocks, dst_num_blocks, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
   return ok();
 }
 
 neo_status neo_debug_validate(const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
                               int32_t max_blocks_per_seq, int32_t block_size, int32_t num_blocks,
                               int32_t* error_count, void* stream) {
-  if (batch < 0) return fail(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   if (batch == 0) return ok();
   if (!block_table || !seq_lens || !error_count)
-    return fail(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || block_size <= 0 || num_blocks <= 0)
-    return fail(NEO_ERR_INVALID_ARG, "sizes must be positive");
+    return set_error(NEO_ERR_INVALID_ARG, "sizes must be positive");
   if ((int64_t)max_blocks_per_seq * block_size >= ((int64_t)1 << 31))
-    return fail(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   hipError_t e = neo::launch_validate(block_table, seq_lens, batch, max_blocks_per_seq,
                                       block_size, num_blocks, error_count,
                                       static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(NEO_ERR_HIP, "validate launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "validate launch: %s", hipGetErrorString(e));
   return ok();
 }
 

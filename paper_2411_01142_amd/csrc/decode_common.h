@@ -249,7 +249,9 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   int32_t found_b = -1, found_p = 0, found_w = 1, found_len = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
     if (p.batch > kChunk) load_weights(p, base, lane, w, raw);
-#pragma unroll
+    // Stops at the register holding the slice start (the first one for
+    // batches up to 64); not unrolled: it runs once per wave.
+#pragma unroll 1
     for (int r = 0; r < kPlanRegs; ++r) {
       if (found_b >= 0) break;
       const int32_t cs = wave_sum_i32(w[r]);
