@@ -205,6 +205,8 @@ constexpr int kPlanRegs = 16;
 // s_waitcnt immediate (gfx9 encoding) that waits for vmcnt == 0 and leaves the
 // export and LDS/scalar counters alone.
 constexpr int kWaitVmcnt0 = 0x0F70;
+// ... that waits for lgkmcnt == 0 (LDS and scalar memory) only.
+constexpr int kWaitLgkmcnt0 = 0xC07F;
 
 // Slices of at least this many positions on average merge within a workgroup
 // through LDS (fused launch).
@@ -683,11 +685,21 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         constexpr int kLdsMergeHeads = GroupMerge<G>::kHeadsPerPass;
         const int ls = partial_slot(wave, si.s0, first_tile) - slot0;
         F::template write<false>(st, gm.o[ls], gm.lse[ls], lane);
+        // LDS operations of a wave complete in order: once this wave's
+        // partial writes are done (lgkmcnt 0), its count follows them, and a
+        // wave that reads the count after it sees the partial. Waiting on LDS
+        // only: an acquire-release atomic would also wait for every vector
+        // memory operation in flight (vmcnt 0), including the empty tile load
+        // queued behind other waves' loads, which costs up to a round trip.
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
         int32_t old = 0;
         if (lane == 0)
-          old = __hip_atomic_fetch_add(&gm.count[c0 - first_slice], 1, __ATOMIC_ACQ_REL,
+          old = __hip_atomic_fetch_add(&gm.count[c0 - first_slice], 1, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (__builtin_amdgcn_readlane(old, 0) == c1 - c0) {
+        old = __builtin_amdgcn_readlane(old, 0);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (old == c1 - c0) {
           if (c1 == c0 + 1) {
             merge_two<G, false, kLdsMergeHeads>(p, &gm.o[0][0], &gm.lse[0][0], b, g,
                                 partial_slot(c0, slice_start(c0, si.W, si.n), first_tile) - slot0,
