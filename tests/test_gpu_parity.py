@@ -303,6 +303,22 @@ def test_group_merge_mixes_contributor_counts(variant):
         assert np.array_equal(a, b), f"fused != two_kernel at {slices} slices"
 
 
+def test_batch_beyond_one_plan_round():
+    # More than 1024 requests: the in-kernel plan reads seq_lens in rounds of
+    # 1024 requests; slices must start in the right request in every round
+    # (the staged schedule computes the same slices in a separate kernel).
+    rng = np.random.default_rng(41)
+    lens = rng.integers(0, 80, 2100)
+    lens[rng.random(2100) < 0.1] = 0
+    case = W.build_case(lens.tolist(), 8, 2, 128, 16, seed=41)
+    ref = oracle.decode_attention(case)
+    for variant in ("valu", "mfma"):
+        a = run(case, variant=variant, schedule="fused")
+        assert_parity(a, ref, f"batch 2100 {variant}")
+        for schedule in ("staged", "two_kernel"):
+            assert np.array_equal(a, run(case, variant=variant, schedule=schedule)), schedule
+
+
 def test_poisoned_slots_do_not_leak():
     lens = [1, 15, 17, 64, 99, 250]
     a = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=True)
