@@ -164,7 +164,7 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
     return set_error(NEO_ERR_INVALID_ARG,
                      "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
                      max_blocks_per_seq, num_blocks);
-  if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCost) * num_kv_heads >= ((int64_t)1 << 31))
+  if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCostLong) * num_kv_heads >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG,
                      "batch * (max_blocks_per_seq + 2) * num_kv_heads must stay below 2^31");
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))

@@ -4,8 +4,8 @@
 // or to a partial slot that is merged afterwards).
 //
 // Work is balanced on a weighted line: each (request, kv head) pair with nb > 0
-// blocks occupies nb + kPairCost positions, its startup cost (q, block ids,
-// pipeline fill) followed by one position per block tile. With W positions in
+// blocks occupies nb + pair_cost(nb) positions, its startup cost (q, block
+// ids, pipeline fill, result write) followed by one position per block tile. With W positions in
 // all and n slices, slice s owns [floor(sW/n), floor((s+1)W/n)) and processes
 // the tiles whose positions fall there. A pair whose tiles cross a slice
 // boundary is "cut": every slice holding some of its tiles writes a partial
@@ -580,8 +580,9 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       continue;
     }
     const int32_t pair_base = pos - x;
-    const int32_t first_tile = pair_base + kPairCost;  // position of block 0
-    const int32_t j = max(0, x - kPairCost);
+    const int32_t cost = pair_cost(nb);
+    const int32_t first_tile = pair_base + cost;  // position of block 0
+    const int32_t j = max(0, x - cost);
     const int32_t jend = min(nb, si.s1 - first_tile);
     if (jend <= j) break;  // the slice ends before this pair's next tile
 
@@ -726,7 +727,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       }
     }
 
-    pos = pair_base + nb + kPairCost;
+    pos = pair_base + nb + cost;
     x = 0;
     if (pos >= si.s1) break;
     if (++g == p.hkv) {

@@ -19,11 +19,22 @@ constexpr int kWavesPerGroup = 4;               // wavefronts per workgroup (256
 constexpr int kPlanThreads = 1024;
 
 // Work plan. Each (request, kv head) pair with nb > 0 blocks occupies
-// nb + kPairCost positions of a weighted line (its startup cost, then one
+// nb + pair_cost(nb) positions of a weighted line (its startup cost, then one
 // position per block tile), pairs in request-major, kv-head-next order; slice
 // s owns positions [starts[s].pos, starts[s+1].pos) and is run by one
-// wavefront.
-constexpr int32_t kPairCost = 2;  // measured: 1-2 best, 4 and 6 slower
+// wavefront. The startup cost is what a wave loses between two pairs, in
+// tiles: about two for a short pair (its rows are written, the next pair's
+// first tile is a round trip away), three for a pair long enough to be cut
+// between slices (a partial is written and counted; the merge follows).
+// Measured: one cost for every pair gives 2 as the best compromise (1 is
+// 2.7 points slower on a mix of short requests, 3 is 0.8 points faster on
+// long requests but 0.6 slower on the short mix).
+constexpr int32_t kPairCost = 2;
+constexpr int32_t kPairCostLong = 3;
+constexpr int32_t kLongPairBlocks = 32;
+__host__ __device__ inline int32_t pair_cost(int32_t nb) {
+  return nb >= kLongPairBlocks ? kPairCostLong : kPairCost;
+}
 
 struct alignas(16) PlanHeader {
   int32_t total;     // positions on the weighted line
@@ -36,7 +47,7 @@ struct alignas(32) SliceStart {
   int32_t pos;  // first position of the slice
   int32_t b;    // request of the pair holding it
   int32_t g;    // kv head of that pair
-  int32_t x;    // offset of pos inside the pair's nb + kPairCost positions
+  int32_t x;    // offset of pos inside the pair's nb + pair_cost(nb) positions
   int32_t nb;   // blocks of that pair
   int32_t pad[3];
 };
@@ -84,7 +95,7 @@ __host__ __device__ inline int32_t blocks_of(int32_t L, int32_t mbps) {
 // Positions of each (request, kv head) pair of a request with this length.
 __host__ __device__ inline int32_t pair_weight(int32_t L, int32_t mbps) {
   const int32_t nb = blocks_of(L, mbps);
-  return nb > 0 ? nb + kPairCost : 0;
+  return nb > 0 ? nb + pair_cost(nb) : 0;
 }
 
 struct DecodeParams {

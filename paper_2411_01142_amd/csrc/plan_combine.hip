@@ -73,7 +73,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       st.b = lo;
       st.g = r / w;
       st.x = r % w;
-      st.nb = w - kPairCost;
+      st.nb = blocks_of(lens[lo], mbps);
     }
     starts[s] = st;
   }
@@ -129,8 +129,9 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeP
     asm volatile("" ::"v"(la[h]), "v"(lb[h]), "v"(oa[h].x), "v"(oa[h].y), "v"(ob[h].x),
                  "v"(ob[h].y));
   if (s >= n) return;
-  if (a.x <= kPairCost) return;                 // no tile of the pair before the boundary
-  const int32_t first_tile = a.pos - a.x + kPairCost;
+  const int32_t cost = pair_cost(a.nb);
+  if (a.x <= cost) return;                      // no tile of the pair before the boundary
+  const int32_t first_tile = a.pos - a.x + cost;
   const int32_t prev_start = slice_start(s - 1, W, n);
   if (first_tile < prev_start) return;          // an earlier boundary cuts it first
   const int32_t c1 = slice_of(first_tile + a.nb - 1, W, n);
