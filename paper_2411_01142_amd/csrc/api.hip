@@ -73,8 +73,8 @@ void* device_address(const void* p) {
 bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
 
 // Compute units of the current device, cached per device ordinal. The default
-// plan uses whole multiples of (CUs x wavefronts per workgroup) slices, up to
-// two workgroups per CU.
+// plan uses at most CUs x wavefronts per workgroup slices (one workgroup per
+// CU).
 constexpr int kMaxDevices = 64;
 std::atomic<int32_t> g_cu_count[kMaxDevices];
 
