@@ -17,6 +17,7 @@ Cache (each replica holds identical values). Prints one JSON line.
     python bench.py --op profile_costs [--out F]   # T_ga / T_ca grids for the cost model
     python bench.py --op schedule_sim [--costs F]  # load-aware scheduler vs GPU-only, simulated
     python bench.py --op overlap_demo              # asymmetric pipelining, measured on the box
+    python bench.py --op read_ceiling              # the device's streaming-read rate (4 GiB)
 """
 from __future__ import annotations
 
@@ -45,6 +46,12 @@ SEQ_DESC = {1: "U[64,512]", 2: "U[512,2048]", 3: "lognormal(median 1500, sigma 0
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def pct(values, qs):
+    """Percentiles (nearest rank) of a list of numbers."""
+    xs = sorted(values)
+    return [xs[min(len(xs) - 1, max(0, math.ceil(q / 100 * len(xs)) - 1))] for q in qs]
 
 
 def kernel_source_sha(variant: str) -> str:
@@ -268,6 +275,41 @@ def bench_kv_op(args, torch, neo, W):
                                    "GBs": round(nbytes / (dms * 1e-3) / 1e9, 2),
                                    "us_per_call": round(dms * 1e3, 3)}
     print(json.dumps(result), flush=True)
+    return 0
+
+
+def bench_read_ceiling(args, torch, neo):
+    """The device's streaming-read rate over 4 GiB (the practical ceiling of an
+    HBM-bound kernel that reads its data once), nontemporal and plain loads."""
+    nbytes = 4 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.empty(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
+    hip = HipEvents()
+    sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    rates = {}
+    for nt in (True, False):
+        for _ in range(2):
+            neo.read_probe(src, sink, nontemporal=nt)
+        ms = []
+        for _ in range(max(args.steps // 10, 5)):
+            a, b = hip.create(), hip.create()
+            hip.record(a, sh)
+            neo.read_probe(src, sink, nontemporal=nt)
+            hip.record(b, sh)
+            torch.cuda.synchronize()
+            ms.append(hip.elapsed_ms(a, b))
+            hip.destroy(a)
+            hip.destroy(b)
+        rates["nontemporal" if nt else "plain"] = [round(nbytes / (m * 1e-3) / 1e9, 1) for m in ms]
+    best = max(max(v) for v in rates.values())
+    med = {k: pct(v, (50,))[0] for k, v in rates.items()}
+    print(json.dumps({
+        "metric": "device streaming-read rate (read ceiling for HBM-bound kernels)",
+        "value": med["nontemporal"], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+        "bytes": nbytes, "median_gbs": med, "best_gbs": best, "runs_gbs": rates,
+        "roofline": {"bound": "hbm", "achieved": med["nontemporal"], "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(med["nontemporal"] / PEAK_HBM_GBS, 4)},
+    }), flush=True)
     return 0
 
 
@@ -558,7 +600,8 @@ def main(argv=None):
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--op", default="decode",
                     choices=["decode", "kv_swap_out", "kv_swap_in", "kv_copy_d2d", "kv_append",
-                             "cpu_decode", "profile_costs", "schedule_sim", "overlap_demo"])
+                             "cpu_decode", "profile_costs", "schedule_sim", "overlap_demo",
+                             "read_ceiling"])
     ap.add_argument("--out", default="")
     ap.add_argument("--costs", default="")
     ap.add_argument("--cpu-threads", type=int, default=0)
@@ -590,6 +633,8 @@ def main(argv=None):
         return bench_profile_costs(args, torch, neo)
     if args.op == "overlap_demo":
         return bench_overlap_demo(args, torch)
+    if args.op == "read_ceiling":
+        return bench_read_ceiling(args, torch, neo)
     if args.op != "decode":
         return bench_kv_op(args, torch, neo, W)
 
@@ -703,8 +748,14 @@ def main(argv=None):
             "traffic": traffic,
             "kernel_ms": round(kernel_ms, 5),
             "kernel_ms_event_pair": round(dec_ms, 5),
+            # Per-call spread of the event pairs around the decode kernel.
+            "kernel_ms_event_pair_p10_p50_p90": [round(x, 5) for x in pct(decode_ms, (10, 50, 90))],
             "gpu_ms_per_step": round(region_ms, 5),
             "algorithmic_bytes_per_launch": alg_bytes,
+            # HBM bytes the counters saw (FETCH + WRITE, copy-calibrated) over the same
+            # kernel time, beside the algorithmic rate above.
+            "achieved_traffic_gbs": (round(traffic / (kernel_ms * 1e-3) / 1e9, 2)
+                                     if traffic else None),
         },
     }
     if not args.no_cpu_baseline:

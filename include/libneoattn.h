@@ -197,6 +197,20 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
  * must be distinct and must not be read by the same call (no in-place chains).
  * head_dim 128, block_size 16; all four caches 16-byte aligned.
  */
+/*
+ * Measurement aid, not part of attention: the device's streaming-read rate,
+ * the practical ceiling for an HBM-bound kernel (the decode kernel reads its
+ * KV once). Reads `bytes` of device memory at `src` once (16-byte loads,
+ * 8 per thread in flight, nontemporal when `nontemporal` != 0) and writes
+ * NEO_READ_PROBE_SINK_WORDS words to `sink` (device memory, caller-owned):
+ * word w is the xor of every 32-bit word wave w read, so the xor of all of
+ * them is the xor of the buffer. One kernel on `stream`; time it with events.
+ * bytes: a positive multiple of 16; src 16-byte aligned.
+ */
+#define NEO_READ_PROBE_SINK_WORDS 16384
+neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, uint32_t* sink,
+                          size_t sink_words, void* stream);
+
 neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                               const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
                               int32_t num_kv_heads, int32_t head_dim, int32_t block_size,

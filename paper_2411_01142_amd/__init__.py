@@ -29,6 +29,7 @@ __all__ = [
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
     "new_workspace", "kv_append", "copy_blocks", "cpu_decode_attention", "CPU_ISAS",
     "cpu_best_isa", "cpu_default_threads", "cpu_read_probe", "cpu_kv_append",
+    "read_probe", "READ_PROBE_SINK_WORDS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -38,6 +39,7 @@ CPU_ISAS = {"auto": 0, "generic": 1, "avx512_bf16": 2, "avx512": 3}
 VARIANTS = {"auto": 0, "valu": 1, "mfma": 2}
 SCHEDULES = {"auto": 0, "fused": 1, "staged": 2, "two_kernel": 3}
 MAX_SLICES = 4096
+READ_PROBE_SINK_WORDS = 16384
 STATUS = {0: "NEO_OK", 1: "NEO_ERR_INVALID_ARG", 2: "NEO_ERR_UNSUPPORTED",
           3: "NEO_ERR_WORKSPACE", 4: "NEO_ERR_HIP"}
 
@@ -94,6 +96,8 @@ def load_library():
         lib.neo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
         lib.neo_kv_append.restype = ctypes.c_int
         lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
+        lib.neo_read_probe.argtypes = [P, S, I, P, S, P]
+        lib.neo_read_probe.restype = ctypes.c_int
         lib.neo_kv_copy_blocks.restype = ctypes.c_int
         lib.neo_cpu_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I, I]
         lib.neo_cpu_decode_attention_ex.restype = ctypes.c_int
@@ -349,6 +353,24 @@ def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, *, stream=None, de
                                       dst_v.data_ptr(), src_ids.data_ptr(), dst_ids.data_ptr(),
                                       src_ids.shape[0], Hkv, npieces * x, bs, NB_s,
                                       dst_k.shape[0], sh))
+
+
+def read_probe(src, sink, *, nontemporal: bool = True, stream=None):
+    """Stream-read the GPU tensor ``src`` once (its bytes, a multiple of 16) and
+    write ``READ_PROBE_SINK_WORDS`` per-wave xor words into ``sink`` (an int32 or
+    uint32-sized GPU tensor): a measurement of the device's read rate. Runs on
+    ``stream`` without synchronising."""
+    torch = _torch()
+    lib = load_library()
+    if not (src.is_cuda and sink.is_cuda) or not src.is_contiguous() or not sink.is_contiguous():
+        raise ValueError("src and sink must be contiguous GPU tensors")
+    if sink.numel() * sink.element_size() < 4 * READ_PROBE_SINK_WORDS:
+        raise ValueError(f"sink must hold {READ_PROBE_SINK_WORDS} 32-bit words")
+    sh = _stream_handle(stream, src.device)
+    with torch.cuda.device(src.device):
+        _check(lib.neo_read_probe(src.data_ptr(), src.numel() * src.element_size(),
+                                  int(bool(nontemporal)), sink.data_ptr(),
+                                  sink.numel() * sink.element_size() // 4, sh))
 
 
 def cpu_best_isa() -> str:

@@ -377,6 +377,23 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
   return ok();
 }
 
+static_assert(neo::kReadProbeWaves == NEO_READ_PROBE_SINK_WORDS, "probe sink size");
+
+neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, uint32_t* sink,
+                          size_t sink_words, void* stream) {
+  if (!src || !sink) return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (bytes == 0 || bytes % 16 != 0)
+    return set_error(NEO_ERR_INVALID_ARG, "bytes (%zu) must be a positive multiple of 16", bytes);
+  if (!aligned(src, 16)) return set_error(NEO_ERR_INVALID_ARG, "src must be 16-byte aligned");
+  if (sink_words < (size_t)NEO_READ_PROBE_SINK_WORDS)
+    return set_error(NEO_ERR_INVALID_ARG, "sink holds %zu words, needs %d", sink_words,
+                     NEO_READ_PROBE_SINK_WORDS);
+  const hipError_t e = neo::launch_read_probe(src, bytes / 16, nontemporal != 0, sink,
+                                              static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "probe launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 neo_status neo_debug_validate(const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
                               int32_t max_blocks_per_seq, int32_t block_size, int32_t num_blocks,
                               int32_t* error_count, void* stream) {

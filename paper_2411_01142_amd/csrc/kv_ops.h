@@ -15,4 +15,11 @@ hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint
                               int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
                               hipStream_t stream);
 
+// Streaming-read probe: reads n16 16-byte words once; sink gets one word per
+// wave (kReadProbeWaves of them), the xor of every 32-bit word that wave read.
+constexpr int kReadProbeBlocks = 4096;
+constexpr int kReadProbeWaves = kReadProbeBlocks * 4;
+hipError_t launch_read_probe(const void* src, size_t n16, bool nontemporal, uint32_t* sink,
+                             hipStream_t stream);
+
 }  // namespace neo

@@ -102,4 +102,49 @@ hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint
   return hipGetLastError();
 }
 
+// ----------------------------------------------------------------- read probe
+
+namespace {
+
+typedef uint32_t probe_u32x4 __attribute__((ext_vector_type(4)));
+
+// Each thread reads words tid, tid + stride, ... with 8 loads in flight, xors
+// them, and the wave's xor goes to sink: the loads cannot be dropped, and the
+// result is checkable (the xor of all sink words is the xor of the buffer).
+template <bool kNontemporal>
+__global__ __launch_bounds__(256) void read_probe_kernel(const probe_u32x4* __restrict__ src,
+                                                         size_t n16, uint32_t* __restrict__ sink) {
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  auto ld = [&](size_t i) -> probe_u32x4 {
+    return kNontemporal ? __builtin_nontemporal_load(src + i) : src[i];
+  };
+  probe_u32x4 acc = {0u, 0u, 0u, 0u};
+  size_t i = tid;
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    probe_u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ld(i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u];
+  }
+  for (; i < n16; i += stride) acc ^= ld(i);
+  uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x ^= __shfl_xor(x, o);
+  if ((threadIdx.x & 63) == 0) sink[tid >> 6] = x;
+}
+
+}  // namespace
+
+hipError_t launch_read_probe(const void* src, size_t n16, bool nontemporal, uint32_t* sink,
+                             hipStream_t stream) {
+  const probe_u32x4* s = static_cast<const probe_u32x4*>(src);
+  if (nontemporal)
+    read_probe_kernel<true><<<kReadProbeBlocks, 256, 0, stream>>>(s, n16, sink);
+  else
+    read_probe_kernel<false><<<kReadProbeBlocks, 256, 0, stream>>>(s, n16, sink);
+  return hipGetLastError();
+}
+
 }  // namespace neo

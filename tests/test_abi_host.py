@@ -189,6 +189,21 @@ def test_kv_copy_blocks_rejects(lib, kw, code):
     assert lib.neo_last_error().decode()
 
 
+@pytest.mark.parametrize("src,nbytes,sink,words", [
+    (None, 16, FAKE, 16384), (FAKE, 16, None, 16384), (FAKE, 0, FAKE, 16384),
+    (FAKE, 24, FAKE, 16384), (FAKE + 8, 16, FAKE, 16384), (FAKE, 16, FAKE, 16383),
+])
+def test_read_probe_rejects(lib, src, nbytes, sink, words):
+    assert lib.neo_read_probe(src, nbytes, 1, sink, words, None) == INVALID
+    assert lib.neo_last_error().decode()
+
+
+def test_read_probe_sink_size_matches_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define NEO_READ_PROBE_SINK_WORDS (\d+)", text).group(1)) == \
+        neo.READ_PROBE_SINK_WORDS
+
+
 def test_kv_copy_blocks_zero_blocks_is_a_noop(lib):
     assert copy_call(lib, n=0, sk=None, sv=None, dk=None, dv=None, si=None, di=None) == OK
 
