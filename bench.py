@@ -65,9 +65,11 @@ def kernel_source_sha(variant: str) -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload_key: str, variant: str, launches_per_step: int = 1):
-    """HBM bytes per decode launch from committed rocprofv3 --pmc summaries, or None
-    when they are missing or were taken on different kernel sources."""
+def load_traffic(workload_key: str, variant: str, launches_per_step: int = 1,
+                 reads_only: bool = False):
+    """HBM bytes per decode launch (read + written, or read only) from committed
+    rocprofv3 --pmc summaries, or None when they are missing or were taken on
+    different kernel sources."""
     path = os.path.join(ROOT, "profiles", f"counters__decode_{variant}__{workload_key}.md")
     if not os.path.exists(path):
         return None
@@ -77,6 +79,8 @@ def load_traffic(workload_key: str, variant: str, launches_per_step: int = 1):
     rec = json.loads(m.group(1))
     if rec.get("kernel_sha") != kernel_source_sha(variant):
         return None
+    if reads_only:
+        return float(rec["fetch_kib_per_launch"]) * 1024 * float(rec["copy_factor_fetch"])
     return float(rec["traffic_bytes_per_launch"])
 
 
@@ -711,6 +715,7 @@ def main(argv=None):
     kernel_ms = region_ms if schedule == "fused" else dec_ms
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     traffic = load_traffic(workload_key, f"{resolved}_{schedule}")
+    fetched = load_traffic(workload_key, f"{resolved}_{schedule}", reads_only=True)
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -756,6 +761,9 @@ def main(argv=None):
             # kernel time, beside the algorithmic rate above.
             "achieved_traffic_gbs": (round(traffic / (kernel_ms * 1e-3) / 1e9, 2)
                                      if traffic else None),
+            # Bytes read only (FETCH_SIZE), the read rate over the same time.
+            "achieved_fetch_gbs": (round(fetched / (kernel_ms * 1e-3) / 1e9, 2)
+                                   if fetched else None),
         },
     }
     if not args.no_cpu_baseline:
