@@ -319,6 +319,48 @@ def test_batch_beyond_one_plan_round():
             assert np.array_equal(a, run(case, variant=variant, schedule=schedule)), schedule
 
 
+def random_case(i):
+    rng = np.random.default_rng(1000 + i)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    group = int(rng.choice([1, 2, 4, 8, 16]))
+    batch = int(rng.integers(1, 301))
+    kind = i % 4  # short, long, mixed, exact block multiples
+    if kind == 0:
+        lens = rng.integers(0, 130, batch)
+    elif kind == 1:
+        lens = rng.integers(500, 3001, batch)
+    elif kind == 2:
+        lens = np.where(rng.random(batch) < 0.1, rng.integers(1000, 3001, batch),
+                        rng.integers(0, 200, batch))
+    else:
+        lens = 16 * rng.integers(0, 120, batch)
+    lens[rng.random(batch) < 0.05] = 0
+    # Keep each case small enough for the oracle (a few M token-heads).
+    while lens.sum() * hkv * group > 4_000_000 and batch > 1:
+        batch //= 2
+        lens = lens[:batch]
+    slices = int(rng.choice([0, 0, 1, 3, 64, 256, 1024, neo.MAX_SLICES]))
+    return W.build_case(lens.tolist(), hkv * group, hkv, 128, 16, seed=2000 + i,
+                        poison=bool(i % 2)), slices
+
+
+@pytest.mark.parametrize("i", range(40))
+def test_random_shapes(i):
+    # Seeded random batches: lengths from empty to 3000 tokens (short, long,
+    # mixed and exact block multiples), groups 1-16, 1-8 kv heads, default or
+    # forced slice counts (so long and short slices, workgroup-local and
+    # workspace merges all occur). Fused must match the oracle and, slice for
+    # slice, the two-kernel schedule bit for bit.
+    case, slices = random_case(i)
+    say(f"[random] case {i}: B={case.batch} Hq={case.num_q_heads} Hkv={case.num_kv_heads} "
+        f"sumL={case.total_tokens()} slices={slices}")
+    ref = oracle.decode_attention(case)
+    a = run(case, variant="mfma", schedule="fused", max_slices=slices)
+    assert_parity(a, ref, f"random {i}")
+    b = run(case, variant="mfma", schedule="two_kernel", max_slices=slices)
+    assert np.array_equal(a, b), f"random {i}: fused != two_kernel"
+
+
 def test_poisoned_slots_do_not_leak():
     lens = [1, 15, 17, 64, 99, 250]
     a = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=True)
