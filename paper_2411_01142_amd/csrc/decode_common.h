@@ -251,24 +251,45 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   int32_t found_b = -1, found_p = 0, found_w = 1, found_len = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
     if (p.batch > kChunk) load_weights(p, base, lane, w, raw);
-    // Stops at the register holding the slice start (the first one for
-    // batches up to 64); not unrolled: it runs once per wave.
-#pragma unroll 1
-    for (int r = 0; r < kPlanRegs; ++r) {
-      if (found_b >= 0) break;
-      const int32_t cs = wave_sum_i32(w[r]);
-      if (carry + cs > u) {
-        const int32_t incl = wave_incl_scan_i32(w[r], lane);
-        const uint64_t hit = __ballot(carry + incl > u);
-        const int first = __ffsll((unsigned long long)hit) - 1;
-        found_b = base + r * kWave + first;
-        found_p = carry + __shfl(incl - w[r], first);
-        found_w = __shfl(w[r], first);
-        found_len = __shfl(raw[r], first);
-      } else {
-        carry += cs;
+    // The register (64 requests) holding position u, then the lane. With one
+    // register in use the first is it; otherwise every register's sum is
+    // reduced at once (independent shuffles pipeline; one register after the
+    // other cost ~0.3 us each at batch 1024).
+    int32_t wr = w[0], rawr = raw[0], rr = 0;
+    if (p.batch - base > kWave) {
+      int32_t cs[kPlanRegs];
+#pragma unroll
+      for (int r = 0; r < kPlanRegs; ++r) cs[r] = w[r];
+#pragma unroll
+      for (int o = kWave / 2; o >= 1; o >>= 1)
+#pragma unroll
+        for (int r = 0; r < kPlanRegs; ++r) cs[r] += __shfl_xor(cs[r], o);
+      rr = -1;
+#pragma unroll
+      for (int r = 0; r < kPlanRegs; ++r) {
+        const int32_t c = uniform(cs[r]);
+        if (rr < 0) {
+          if (carry + c > u) rr = r; else carry += c;
+        }
       }
+      if (rr < 0) continue;  // past this round: carry holds its total
+#pragma unroll
+      for (int r = 0; r < kPlanRegs; ++r)
+        if (r == rr) {
+          wr = w[r];
+          rawr = raw[r];
+        }
+    } else if (carry + wave_sum_i32(wr) <= u) {
+      carry += wave_sum_i32(wr);
+      continue;
     }
+    const int32_t incl = wave_incl_scan_i32(wr, lane);
+    const uint64_t hit = __ballot(carry + incl > u);
+    const int first = __ffsll((unsigned long long)hit) - 1;
+    found_b = base + rr * kWave + first;
+    found_p = carry + __shfl(incl - wr, first);
+    found_w = __shfl(wr, first);
+    found_len = __shfl(rawr, first);
   }
   // The request's weight and length come from the registers already loaded:
   // no second round trip to seq_lens before the first table row.
