@@ -97,12 +97,13 @@ __device__ inline void wait_all_memory() {
 
 // ----------------------------------------------------------------- slice geometry
 
-__device__ inline int32_t slice_start(int64_t s, int32_t W, int32_t n) {
-  return (int32_t)((s * W) / n);
+// Geometry of a wave-uniform slice index or position, kept in scalar
+// registers (the fp32 estimate runs on the vector ALU).
+__device__ inline int32_t slice_start_u(int32_t s, const SliceGeom& g) {
+  return uniform(slice_start(s, g));
 }
-// The slice holding position x: the largest s with floor(sW/n) <= x.
-__device__ inline int32_t slice_of(int32_t x, int32_t W, int32_t n) {
-  return (int32_t)((((int64_t)x + 1) * n - 1) / W);
+__device__ inline int32_t slice_of_u(int32_t x, const SliceGeom& g) {
+  return uniform(slice_of(x, g));
 }
 // Partial slot of slice s for a pair whose first tile sits at position
 // first_tile: 2s when that tile is at or before the slice start (the pair runs
@@ -131,7 +132,7 @@ __host__ __device__ inline int32_t slice_count(int32_t W, int32_t min_tiles, int
 }
 
 struct SliceInfo {
-  int32_t W, n;      // total positions, slices
+  SliceGeom geo;     // total positions, slices
   int32_t s0, s1;    // this slice's position range
   int32_t b, g, x;   // pair holding position s0 and the offset of s0 inside it
   int32_t L;         // clamped length of request b, or -1 when the plan does not hold it
@@ -142,9 +143,20 @@ struct SliceInfo {
 // The plan is the same in every lane; saying so lets the compiler keep the
 // slice walk in scalar registers (tile addresses must be scalar for buffer
 // resources).
+__device__ inline float uniform_f32(float v) {
+  return __builtin_bit_cast(float, uniform(__builtin_bit_cast(int32_t, v)));
+}
+__device__ inline SliceGeom make_uniform(SliceGeom g) {
+  g.W = uniform(g.W);
+  g.n = uniform(g.n);
+  g.a = uniform(g.a);
+  g.r = uniform(g.r);
+  g.inv_n = uniform_f32(g.inv_n);
+  g.n_over_w = uniform_f32(g.n_over_w);
+  return g;
+}
 __device__ inline SliceInfo make_uniform(SliceInfo si) {
-  si.W = uniform(si.W);
-  si.n = uniform(si.n);
+  si.geo = make_uniform(si.geo);
   si.s0 = uniform(si.s0);
   si.s1 = uniform(si.s1);
   si.b = uniform(si.b);
@@ -183,9 +195,8 @@ __device__ inline int32_t wave_incl_scan_i32(int32_t v, int lane) {
 // Slice from the plan kernel's output (staged launch).
 __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
   SliceInfo si;
-  si.W = p.hdr->total;
-  si.n = p.hdr->n_slices;
-  if (wave >= si.n) return si;
+  si.geo = make_slice_geom(p.hdr->total, p.hdr->n_slices);
+  if (wave >= si.geo.n) return si;
   const SliceStart a = p.starts[wave];
   si.s0 = a.pos;
   si.s1 = p.starts[wave + 1].pos;
@@ -239,11 +250,12 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
     for (int r = 0; r < kPlanRegs; ++r) s += w[r];
     total += wave_sum_i32(s);
   }
-  si.W = uniform(total * p.hkv);
-  si.n = slice_count(si.W, p.min_tiles, p.max_slices, p.slice_quantum);
-  if (wave >= si.n) return si;
-  si.s0 = slice_start(wave, si.W, si.n);
-  si.s1 = slice_start((int64_t)wave + 1, si.W, si.n);
+  const int32_t W = uniform(total * p.hkv);
+  si.geo = make_uniform(
+      make_slice_geom(W, slice_count(W, p.min_tiles, p.max_slices, p.slice_quantum)));
+  if (wave >= si.geo.n) return si;
+  si.s0 = slice_start_u(wave, si.geo);
+  si.s1 = slice_start_u(wave + 1, si.geo);
 
   // Request b holds positions [hkv*P_b, hkv*P_{b+1}) with P the weight prefix sum.
   const int32_t u = si.s0 / p.hkv;
@@ -351,7 +363,7 @@ template <int G, int GH, bool kCoherent, int kMaxBatch>
 __device__ inline void merge_pair_heads(const DecodeParams& p, const float* part_o,
                                         const float* part_lse, int32_t slot0, int32_t b,
                                         int32_t g, int h0, int32_t first_tile, int32_t c0,
-                                        int32_t c1, int32_t W, int32_t n, int lane) {
+                                        int32_t c1, const SliceGeom& geo, int lane) {
   constexpr int kFit = 32 / GH > 0 ? 32 / GH : 1;  // 64 registers of rows
   constexpr int kBatch = kFit < kMaxBatch ? kFit : kMaxBatch;
   auto ld = [](const float* a) -> float { return kCoherent ? load_coherent(a) : *a; };
@@ -374,7 +386,7 @@ __device__ inline void merge_pair_heads(const DecodeParams& p, const float* part
       for (int u = 0; u < kBatch; ++u) {
         if (!clamp && i0 + u >= cnt) break;  // uniform
         const int c = c0 + base + min(i0 + u, cnt - 1);
-        const int slot = partial_slot(c, slice_start(c, W, n), first_tile) - slot0;
+        const int slot = partial_slot(c, slice_start_u(c, geo), first_tile) - slot0;
 #pragma unroll
         for (int h = 0; h < GH; ++h) {
           const float2 v = ld2(part_o + ((size_t)slot * G + h0 + h) * kHeadDim + d);
@@ -385,7 +397,7 @@ __device__ inline void merge_pair_heads(const DecodeParams& p, const float* part
     };
     load_rows(0, true);
     const int mine = c0 + base + (lane < cnt ? lane : 0);
-    const int my_slot = partial_slot(mine, slice_start(mine, W, n), first_tile) - slot0;
+    const int my_slot = partial_slot(mine, slice_start(mine, geo), first_tile) - slot0;
     // Every head's log-sum-exp is loaded before any cross-lane step, so the
     // loads share one round trip.
     float lse_h[GH];
@@ -432,12 +444,12 @@ __device__ inline void merge_pair_heads(const DecodeParams& p, const float* part
 template <int G, bool kCoherent, int kMaxBatch = 16, int GH = G>
 __device__ inline void merge_pair(const DecodeParams& p, const float* part_o,
                                   const float* part_lse, int32_t slot0, int32_t b, int32_t g,
-                                  int32_t first_tile, int32_t c0, int32_t c1, int32_t W,
-                                  int32_t n, int lane) {
+                                  int32_t first_tile, int32_t c0, int32_t c1,
+                                  const SliceGeom& geo, int lane) {
   static_assert(G % GH == 0, "head passes must tile the group");
   for (int h0 = 0; h0 < G; h0 += GH)
     merge_pair_heads<G, GH, kCoherent, kMaxBatch>(p, part_o, part_lse, slot0, b, g, h0,
-                                                  first_tile, c0, c1, W, n, lane);
+                                                  first_tile, c0, c1, geo, lane);
 }
 
 // The merge of a pair with exactly two contributors, partial slots sa (the
@@ -534,7 +546,8 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   // of several tiles; for tiny slices the barrier that clears the counters
   // costs more than it saves. The plan is the same in every wave of the block,
   // so all of them take (or skip) the barrier, before any returns.
-  const bool group_merge = kMergeHere && si.n > 0 && si.W >= kGroupMergeMinTiles * si.n;
+  const bool group_merge =
+      kMergeHere && si.geo.n > 0 && si.geo.W >= kGroupMergeMinTiles * si.geo.n;
   if constexpr (kMergeHere) {
     if (group_merge) {
       if (threadIdx.x < kWavesPerGroup) gm.count[threadIdx.x] = 0;
@@ -543,7 +556,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
   }
   if (kSched == kTwoKernel && lane == 0) {
     // Record the plan for the combine kernel.
-    if (wave < si.n) {
+    if (wave < si.geo.n) {
       SliceStart a;
       a.pos = si.s0;
       a.b = si.b;
@@ -555,20 +568,20 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     }
     if (wave == 0) {
       SliceStart e;
-      e.pos = si.W;
+      e.pos = si.geo.W;
       e.b = p.batch;
       e.g = e.x = e.nb = 0;
       e.pad[0] = e.pad[1] = e.pad[2] = 0;
-      p.starts[si.n] = e;
+      p.starts[si.geo.n] = e;
       PlanHeader h;
-      h.total = si.W;
-      h.n_slices = si.n;
+      h.total = si.geo.W;
+      h.n_slices = si.geo.n;
       h.batch = p.batch;
       h.pad = 0;
       *p.hdr = h;
     }
   }
-  if (wave >= si.n) return;
+  if (wave >= si.geo.n) return;
 
   __shared__ typename F::Shared shared[kWavesPerGroup];
   typename F::Shared& sh = shared[wv];
@@ -666,7 +679,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     if constexpr (kMergeHere && F::kFastMerge)
       fast_cand = j == 0 && jend < nb &&
                   (!group_merge || wave + 1 == first_slice + kWavesPerGroup) &&
-                  slice_of(first_tile + nb - 1, si.W, si.n) == wave + 1;
+                  slice_of_u(first_tile + nb - 1, si.geo) == wave + 1;
     const int32_t check_at = fast_cand ? max(j, jend - kMergeCheckAhead) : -1;
     int32_t seen = 0;
     for (int32_t jj = j; jj < jend; jj += PF + 1) {
@@ -693,16 +706,16 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         if (lane == 0)
           __hip_atomic_store(p.counters + wave, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const int32_t nxt = wave + 1;
-        const int slot = partial_slot(nxt, slice_start(nxt, si.W, si.n), first_tile);
+        const int slot = partial_slot(nxt, slice_start_u(nxt, si.geo), first_tile);
         F::merge_write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
                        p.out + ((size_t)b * p.hq + g * G) * kHeadDim, lane);
       }
-    } else if (group_merge && slice_of(first_tile, si.W, si.n) >= first_slice &&
-               slice_of(first_tile + nb - 1, si.W, si.n) < first_slice + kWavesPerGroup) {
+    } else if (group_merge && slice_of_u(first_tile, si.geo) >= first_slice &&
+               slice_of_u(first_tile + nb - 1, si.geo) < first_slice + kWavesPerGroup) {
       if constexpr (kMergeHere) {
         // Every contributor is a wave of this workgroup: merge through LDS.
-        const int32_t c0 = slice_of(first_tile, si.W, si.n);
-        const int32_t c1 = slice_of(first_tile + nb - 1, si.W, si.n);
+        const int32_t c0 = slice_of_u(first_tile, si.geo);
+        const int32_t c1 = slice_of_u(first_tile + nb - 1, si.geo);
         const int32_t slot0 = 2 * first_slice;
         constexpr int kLdsMergeHeads = GroupMerge<G>::kHeadsPerPass;
         const int ls = partial_slot(wave, si.s0, first_tile) - slot0;
@@ -724,12 +737,12 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         if (old == c1 - c0) {
           if (c1 == c0 + 1) {
             merge_two<G, false, kLdsMergeHeads>(p, &gm.o[0][0], &gm.lse[0][0], b, g,
-                                partial_slot(c0, slice_start(c0, si.W, si.n), first_tile) - slot0,
-                                partial_slot(c1, slice_start(c1, si.W, si.n), first_tile) - slot0,
+                                partial_slot(c0, slice_start_u(c0, si.geo), first_tile) - slot0,
+                                partial_slot(c1, slice_start_u(c1, si.geo), first_tile) - slot0,
                                 lane);
           } else {
             merge_pair<G, false, 1, kLdsMergeHeads>(p, &gm.o[0][0], &gm.lse[0][0], slot0, b, g,
-                                                    first_tile, c0, c1, si.W, si.n, lane);
+                                                    first_tile, c0, c1, si.geo, lane);
           }
         }
       }
@@ -738,8 +751,8 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       F::template write<kMergeHere>(st, p.part_o + (size_t)slot * G * kHeadDim,
                                 p.part_lse + slot * G, lane);
       if (kMergeHere) {
-        const int32_t c0 = slice_of(first_tile, si.W, si.n);
-        const int32_t c1 = slice_of(first_tile + nb - 1, si.W, si.n);
+        const int32_t c0 = slice_of_u(first_tile, si.geo);
+        const int32_t c1 = slice_of_u(first_tile + nb - 1, si.geo);
         if (arrive_last(p, c0, c1, lane)) {
           const Pending rec{b, g, first_tile, c0, c1};
           if (npend == 0) pend0 = rec; else pend1 = rec;
@@ -761,11 +774,11 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       const Pending q = i == 0 ? pend0 : pend1;
       if (q.c1 == q.c0 + 1) {
         merge_two<G, true>(p, p.part_o, p.part_lse, q.b, q.g,
-                           partial_slot(q.c0, slice_start(q.c0, si.W, si.n), q.first),
-                           partial_slot(q.c1, slice_start(q.c1, si.W, si.n), q.first), lane);
+                           partial_slot(q.c0, slice_start_u(q.c0, si.geo), q.first),
+                           partial_slot(q.c1, slice_start_u(q.c1, si.geo), q.first), lane);
       } else {
-        merge_pair<G, true>(p, p.part_o, p.part_lse, 0, q.b, q.g, q.first, q.c0, q.c1, si.W,
-                            si.n, lane);
+        merge_pair<G, true>(p, p.part_o, p.part_lse, 0, q.b, q.g, q.first, q.c0, q.c1, si.geo,
+                            lane);
       }
     }
   }

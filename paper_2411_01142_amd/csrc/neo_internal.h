@@ -36,6 +36,50 @@ __host__ __device__ inline int32_t pair_cost(int32_t nb) {
   return nb >= kLongPairBlocks ? kPairCostLong : kPairCost;
 }
 
+// Slice geometry of the weighted line: W positions cut into n slices, slice s
+// owning [floor(sW/n), floor((s+1)W/n)). Evaluated without 64-bit division,
+// which the GPU has no instruction for (the software sequence would run at
+// every pair transition and merge): with W = a n + r, floor(sW/n) =
+// s a + floor(s r / n), where s r < n^2 <= 2^24 is exact in fp32; the fp32
+// quotient is within one of that floor and one exact integer step corrects it.
+struct SliceGeom {
+  int32_t W, n;     // positions and slices, 0 < n <= min(W, NEO_MAX_SLICES) (n = 0: no slices)
+  int32_t a, r;     // W = a n + r
+  float inv_n;      // 1 / n
+  float n_over_w;   // n / W
+};
+static_assert((int64_t)NEO_MAX_SLICES * NEO_MAX_SLICES <= (int64_t)1 << 24,
+              "s r must be exact in fp32");
+
+__host__ __device__ inline SliceGeom make_slice_geom(int32_t W, int32_t n) {
+  SliceGeom g;
+  g.W = W;
+  g.n = n;
+  g.a = n > 0 ? W / n : 0;
+  g.r = W - g.a * n;
+  g.inv_n = n > 0 ? 1.f / (float)n : 0.f;
+  g.n_over_w = W > 0 ? (float)n / (float)W : 0.f;
+  return g;
+}
+// floor(sW/n), for 0 <= s <= n.
+__host__ __device__ inline int32_t slice_start(int32_t s, const SliceGeom& g) {
+  const int32_t sr = s * g.r;
+  int32_t q = (int32_t)((float)sr * g.inv_n);
+  const int32_t t = sr - q * g.n;
+  q += t < 0 ? -1 : (t >= g.n ? 1 : 0);
+  return s * g.a + q;
+}
+// The slice holding position x, 0 <= x < W: the largest s with
+// slice_start(s) <= x, i.e. ceil((x+1) n / W) - 1. The fp32 estimate of
+// (x+1) n / W is within 2^-10 of it, so its floor is off by at most one.
+__host__ __device__ inline int32_t slice_of(int32_t x, const SliceGeom& g) {
+  int32_t s = (int32_t)(((float)x + 1.f) * g.n_over_w);
+  s = s < g.n - 1 ? s : g.n - 1;
+  if (slice_start(s, g) > x) --s;
+  else if (s + 1 < g.n && slice_start(s + 1, g) <= x) ++s;
+  return s;
+}
+
 struct alignas(16) PlanHeader {
   int32_t total;     // positions on the weighted line
   int32_t n_slices;

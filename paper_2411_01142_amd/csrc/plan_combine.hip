@@ -51,6 +51,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   const int32_t* pre = in_lds ? sprefix : prefix;
 
   const int32_t n = slice_count(total, min_tiles, max_slices, quantum);
+  const SliceGeom geo = make_slice_geom(total, n);
   for (int s = tid; s <= n; s += kPlanThreads) {
     SliceStart st;
     st.pad[0] = st.pad[1] = st.pad[2] = 0;
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       st.x = 0;
       st.nb = 0;
     } else {
-      const int32_t pos = slice_start(s, total, n);
+      const int32_t pos = slice_start(s, geo);
       int lo = 0, hi = batch - 1;  // largest b with pre[b] <= pos
       while (lo < hi) {
         int mid = (lo + hi + 1) >> 1;
@@ -132,14 +133,15 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeP
   const int32_t cost = pair_cost(a.nb);
   if (a.x <= cost) return;                      // no tile of the pair before the boundary
   const int32_t first_tile = a.pos - a.x + cost;
-  const int32_t prev_start = slice_start(s - 1, W, n);
+  const SliceGeom geo = make_slice_geom(W, n);
+  const int32_t prev_start = slice_start(s - 1, geo);
   if (first_tile < prev_start) return;          // an earlier boundary cuts it first
-  const int32_t c1 = slice_of(first_tile + a.nb - 1, W, n);
+  const int32_t c1 = slice_of(first_tile + a.nb - 1, geo);
   if (c1 == s && first_tile > prev_start) {
     merge_two_values<G>(p, a.b, a.g, la, lb, oa, ob, lane);  // slots 2s-1, 2s
     return;
   }
-  merge_pair<G, false>(p, p.part_o, p.part_lse, 0, a.b, a.g, first_tile, s - 1, c1, W, n, lane);
+  merge_pair<G, false>(p, p.part_o, p.part_lse, 0, a.b, a.g, first_tile, s - 1, c1, geo, lane);
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* __restrict__ dst, size_t words) {
