@@ -48,12 +48,13 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 // the mapped device address for pinned host memory, NULL for anything else
 // (pageable host memory, unknown pointers). Clears the error HIP records for
 // an unknown pointer.
-void* device_address(const void* p) {
+void* device_address(const void* p, bool* in_device_memory = nullptr) {
   hipPointerAttribute_t a;
   if (hipPointerGetAttributes(&a, p) != hipSuccess) {
     (void)hipGetLastError();
     return nullptr;
   }
+  if (in_device_memory) *in_device_memory = a.type == hipMemoryTypeDevice;
   switch (a.type) {
     case hipMemoryTypeDevice:
     case hipMemoryTypeManaged:
@@ -360,9 +361,10 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
   // memory; pageable host memory would fault the kernel, so it is refused here.
   const void* ptrs[6] = {src_k, src_v, dst_k, dst_v, src_ids, dst_ids};
   void* dev[6];
+  bool in_hbm[6];
   static const char* names[6] = {"src_k", "src_v", "dst_k", "dst_v", "src_ids", "dst_ids"};
   for (int i = 0; i < 6; ++i) {
-    dev[i] = device_address(ptrs[i]);
+    dev[i] = device_address(ptrs[i], &in_hbm[i]);
     if (!dev[i])
       return set_error(NEO_ERR_INVALID_ARG,
                        "%s is not device memory or pinned host memory the device can address",
@@ -372,7 +374,7 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
       static_cast<const uint16_t*>(dev[0]), static_cast<const uint16_t*>(dev[1]),
       static_cast<uint16_t*>(dev[2]), static_cast<uint16_t*>(dev[3]),
       static_cast<const int32_t*>(dev[4]), static_cast<const int32_t*>(dev[5]), n, num_kv_heads,
-      src_num_blocks, dst_num_blocks, static_cast<hipStream_t>(stream));
+      src_num_blocks, dst_num_blocks, in_hbm[2] && in_hbm[3], static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
   return ok();
 }

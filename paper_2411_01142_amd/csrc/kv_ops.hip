@@ -43,7 +43,11 @@ __global__ __launch_bounds__(128) void append_kernel(
 
 // One workgroup per copied block: K and V, 16 bytes per access, four words of
 // each cache loaded before any is stored so that reads over the host link
-// keep eight requests in flight per thread.
+// keep eight requests in flight per thread. Every byte is touched once, so
+// loads (and stores into device memory) are nontemporal: a block copy between
+// two HBM caches measured 5.9 TB/s (read + write) against 5.3 with cached
+// accesses.
+template <bool kStreamStores>
 __global__ __launch_bounds__(256) void copy_blocks_kernel(
     const uint16_t* __restrict__ src_k, const uint16_t* __restrict__ src_v,
     uint16_t* __restrict__ dst_k, uint16_t* __restrict__ dst_v,
@@ -67,16 +71,21 @@ __global__ __launch_bounds__(256) void copy_blocks_kernel(
     for (int u = 0; u < kUnroll; ++u) {
       if (u < rows) {
         const int w = w0 + u * 256 + threadIdx.x;
-        a[u] = sk[w];
-        c[u] = sv[w];
+        a[u] = __builtin_nontemporal_load(sk + w);
+        c[u] = __builtin_nontemporal_load(sv + w);
       }
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       if (u < rows) {
         const int w = w0 + u * 256 + threadIdx.x;
-        dk[w] = a[u];
-        dv[w] = c[u];
+        if (kStreamStores) {
+          __builtin_nontemporal_store(a[u], dk + w);
+          __builtin_nontemporal_store(c[u], dv + w);
+        } else {
+          dk[w] = a[u];
+          dv[w] = c[u];
+        }
       }
     }
   }
@@ -96,9 +105,13 @@ hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t
 hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
                               uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
                               int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
-                              hipStream_t stream) {
-  copy_blocks_kernel<<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, hkv,
-                                            src_blocks, dst_blocks);
+                              bool dst_in_hbm, hipStream_t stream) {
+  if (dst_in_hbm)
+    copy_blocks_kernel<true><<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids, dst_ids,
+                                                    hkv, src_blocks, dst_blocks);
+  else
+    copy_blocks_kernel<false><<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids,
+                                                     dst_ids, hkv, src_blocks, dst_blocks);
   return hipGetLastError();
 }
 
