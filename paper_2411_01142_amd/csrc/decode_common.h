@@ -166,28 +166,58 @@ __device__ inline SliceInfo make_uniform(SliceInfo si) {
   return si;
 }
 
-__device__ inline int32_t wave_sum_i32(int32_t v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+// Cross-lane arithmetic through DPP (operand modifiers of ordinary vector
+// instructions) rather than shuffles, each of which is a round trip through
+// the LDS crossbar: a 64-lane scan is four shifts inside each 16-lane row and
+// two broadcasts from one row to the next. Measured: the plan's chain of
+// shuffle reductions and scans took ~1.3 us per wave at any batch size.
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowShr2 = 0x112;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142;  // lane 15 of each row to the next row
+constexpr int kDppRowBcast31 = 0x143;  // lane 31 to rows 2 and 3
+
+// v moved by the DPP pattern; lanes with no source (outside the row, or rows
+// left out by kRowMask) get `identity`.
+template <int kCtrl, int kRowMask = 0xF>
+__device__ inline int32_t dpp_move(int32_t identity, int32_t v) {
+  return __builtin_amdgcn_update_dpp(identity, v, kCtrl, kRowMask, 0xF, false);
+}
+// Inclusive scan over the 64 lanes with an associative op and its identity.
+template <class Op>
+__device__ inline int32_t wave_scan_bits(int32_t v, int32_t identity, Op op) {
+  v = op(v, dpp_move<kDppRowShr1>(identity, v));
+  v = op(v, dpp_move<kDppRowShr2>(identity, v));
+  v = op(v, dpp_move<kDppRowShr4>(identity, v));
+  v = op(v, dpp_move<kDppRowShr8>(identity, v));
+  v = op(v, dpp_move<kDppRowBcast15, 0xA>(identity, v));
+  v = op(v, dpp_move<kDppRowBcast31, 0xC>(identity, v));
   return v;
+}
+__device__ inline int32_t wave_incl_scan_i32(int32_t v) {
+  return wave_scan_bits(v, 0, [](int32_t a, int32_t b) { return a + b; });
+}
+// Reductions: the scan's last lane, read into a scalar register.
+__device__ inline int32_t wave_sum_i32(int32_t v) {
+  return __builtin_amdgcn_readlane(wave_incl_scan_i32(v), kWave - 1);
 }
 __device__ inline float wave_max_f32(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  const int32_t s = wave_scan_bits(
+      __builtin_bit_cast(int32_t, v), __builtin_bit_cast(int32_t, -INFINITY),
+      [](int32_t a, int32_t b) {
+        return __builtin_bit_cast(int32_t,
+                                  fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
+      });
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, kWave - 1));
 }
 __device__ inline float wave_sum_f32(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ inline int32_t wave_incl_scan_i32(int32_t v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int32_t u = __shfl_up(v, o);
-    if (lane >= o) v += u;
-  }
-  return v;
+  const int32_t s = wave_scan_bits(
+      __builtin_bit_cast(int32_t, v), 0, [](int32_t a, int32_t b) {
+        return __builtin_bit_cast(int32_t,
+                                  __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+      });
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, kWave - 1));
 }
 
 // ----------------------------------------------------------------- planning
@@ -265,17 +295,14 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
     if (p.batch > kChunk) load_weights(p, base, lane, w, raw);
     // The register (64 requests) holding position u, then the lane. With one
     // register in use the first is it; otherwise every register's sum is
-    // reduced at once (independent shuffles pipeline; one register after the
-    // other cost ~0.3 us each at batch 1024).
+    // reduced at once (the independent reductions pipeline).
     int32_t wr = w[0], rawr = raw[0], rr = 0;
     if (p.batch - base > kWave) {
       int32_t cs[kPlanRegs];
 #pragma unroll
       for (int r = 0; r < kPlanRegs; ++r) cs[r] = w[r];
 #pragma unroll
-      for (int o = kWave / 2; o >= 1; o >>= 1)
-#pragma unroll
-        for (int r = 0; r < kPlanRegs; ++r) cs[r] += __shfl_xor(cs[r], o);
+      for (int r = 0; r < kPlanRegs; ++r) cs[r] = wave_sum_i32(cs[r]);
       rr = -1;
 #pragma unroll
       for (int r = 0; r < kPlanRegs; ++r) {
@@ -295,13 +322,13 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
       carry += wave_sum_i32(wr);
       continue;
     }
-    const int32_t incl = wave_incl_scan_i32(wr, lane);
+    const int32_t incl = wave_incl_scan_i32(wr);
     const uint64_t hit = __ballot(carry + incl > u);
     const int first = __ffsll((unsigned long long)hit) - 1;
     found_b = base + rr * kWave + first;
-    found_p = carry + __shfl(incl - wr, first);
-    found_w = __shfl(wr, first);
-    found_len = __shfl(rawr, first);
+    found_p = carry + __builtin_amdgcn_readlane(incl - wr, first);
+    found_w = __builtin_amdgcn_readlane(wr, first);
+    found_len = __builtin_amdgcn_readlane(rawr, first);
   }
   // The request's weight and length come from the registers already loaded:
   // no second round trip to seq_lens before the first table row.
@@ -423,7 +450,8 @@ __device__ inline void merge_pair_heads(const DecodeParams& p, const float* part
         if (i0 + u >= cnt) break;
 #pragma unroll
         for (int h = 0; h < GH; ++h) {
-          const float wi = __shfl(w[h], i0 + u);
+          const float wi = __builtin_bit_cast(
+              float, __builtin_amdgcn_readlane(__builtin_bit_cast(int32_t, w[h]), i0 + u));
           a0[h] = fmaf(wi, ov[u][h][0], a0[h]);
           a1[h] = fmaf(wi, ov[u][h][1], a1[h]);
         }
@@ -493,7 +521,7 @@ __device__ inline bool arrive_last(const DecodeParams& p, int32_t c0, int32_t c1
   int32_t old = 0;
   if (lane == 0)
     old = __hip_atomic_fetch_add(p.counters + c0, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  old = __shfl(old, 0);
+  old = __builtin_amdgcn_readlane(old, 0);
   if (old != c1 - c0) return false;
   if (lane == 0)
     __hip_atomic_store(p.counters + c0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
