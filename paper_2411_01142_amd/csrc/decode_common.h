@@ -220,6 +220,37 @@ __device__ inline float wave_sum_f32(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, kWave - 1));
 }
 
+// Lane l combined with lane l ^ 16 (resp. l ^ 32) through the gfx950 row swap
+// instructions, no LDS round trip: with the same value in both operands, the
+// first result holds lane (l & ~16)'s value and the second lane (l | 16)'s, so
+// both partners get op(lower lane's value, upper lane's value), the same bits.
+// The results are copied to scalars before the bit cast: a cast applied to a
+// vector-element subscript directly has been lowered as a read of element 0.
+template <class Op>
+__device__ inline float combine_xor16(float v, Op op) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const uint32_t lo = r[0], hi = r[1];
+  return op(__builtin_bit_cast(float, lo), __builtin_bit_cast(float, hi));
+}
+template <class Op>
+__device__ inline float combine_xor32(float v, Op op) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t lo = r[0], hi = r[1];
+  return op(__builtin_bit_cast(float, lo), __builtin_bit_cast(float, hi));
+}
+// Max / sum over the four lanes l, l^16, l^32, l^48 (one column of the
+// 16 x 16 MFMA accumulator layout, or one head's four lane groups).
+__device__ inline float max_over_rows(float v) {
+  const auto mx = [](float a, float b) { return fmaxf(a, b); };
+  return combine_xor32(combine_xor16(v, mx), mx);
+}
+__device__ inline float sum_over_rows(float v) {
+  const auto add = [](float a, float b) { return a + b; };
+  return combine_xor32(combine_xor16(v, add), add);
+}
+
 // ----------------------------------------------------------------- planning
 
 // Slice from the plan kernel's output (staged launch).

@@ -99,8 +99,7 @@ struct MfmaFamily {
           if (4 * rq + i >= valid) x.v[mb][i] = 0;
     }
     float mt = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    mt = max_over_rows(mt);
     const float mn = fmaxf(st.m, mt);  // finite: every tile has a valid token
     const float alpha = __builtin_amdgcn_exp2f(st.m - mn);
     float pr[4];
@@ -131,8 +130,7 @@ struct MfmaFamily {
   __device__ static void write(const State& st, float* __restrict__ rows,
                                float* __restrict__ lse, int lane) {
     const int col = lane & 15, rq = lane >> 4;
-    float lt = st.l + __shfl_xor(st.l, 16);
-    lt += __shfl_xor(lt, 32);
+    const float lt = sum_over_rows(st.l);
     const float inv = 1.f / lt;
     if (col < G) {
       float* r = rows + col * kHeadDim + 4 * rq;
@@ -161,8 +159,7 @@ struct MfmaFamily {
                                      const float* __restrict__ other_lse,
                                      float* __restrict__ out_rows, int lane) {
     const int col = lane & 15, rq = lane >> 4;
-    float lt = st.l + __shfl_xor(st.l, 16);
-    lt += __shfl_xor(lt, 32);
+    const float lt = sum_over_rows(st.l);
     const float inv = 1.f / lt;
     if (col < G) {
       // Rounded exactly as the stored log-sum-exp of write(): the empty asm

@@ -116,8 +116,7 @@ struct ValuFamily {
         s[i][h] = (4 * i + r < valid) ? s[i][h] * scale_log2 : -INFINITY;
         mt = fmaxf(mt, s[i][h]);
       }
-      mt = fmaxf(mt, __shfl_xor(mt, 16));
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      mt = max_over_rows(mt);
       const float mn = fmaxf(st.m[h], mt);
       alpha[h] = __builtin_amdgcn_exp2f(st.m[h] - mn);
       st.m[h] = mn;
@@ -171,8 +170,7 @@ struct ValuFamily {
                                float* __restrict__ lse, int lane) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      float lt = st.l[h] + __shfl_xor(st.l[h], 16);
-      lt += __shfl_xor(lt, 32);
+      const float lt = sum_over_rows(st.l[h]);
       const float inv = 1.f / lt;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
