@@ -28,12 +28,19 @@ constexpr int kPlanThreads = 1024;
 // between slices (a partial is written and counted; the merge follows).
 // Measured: one cost for every pair gives 2 as the best compromise (1 is
 // 2.7 points slower on a mix of short requests, 3 is 0.8 points faster on
-// long requests but 0.6 slower on the short mix).
+// long requests but 0.6 slower on the short mix). On a mix of 1016 short
+// requests, the waves holding them ended ~10 us before those streaming the
+// long ones: a short pair's startup measured ~1.7 tiles. A cost of 1 for the
+// shortest pairs (fewer than 4 blocks) brings the mix's average close to
+// that: +0.2 points there (2 for pairs below 3 blocks: -0.2; below 6: +0.1).
 constexpr int32_t kPairCost = 2;
+constexpr int32_t kPairCostShort = 1;
 constexpr int32_t kPairCostLong = 3;
+constexpr int32_t kShortPairBlocks = 4;
 constexpr int32_t kLongPairBlocks = 32;
 __host__ __device__ inline int32_t pair_cost(int32_t nb) {
-  return nb >= kLongPairBlocks ? kPairCostLong : kPairCost;
+  return nb >= kLongPairBlocks ? kPairCostLong
+                               : (nb >= kShortPairBlocks ? kPairCost : kPairCostShort);
 }
 
 // Slice geometry of the weighted line: W positions cut into n slices, slice s
