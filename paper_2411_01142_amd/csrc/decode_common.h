@@ -293,7 +293,8 @@ constexpr int32_t kMergeCheckAhead = 3;
 __device__ inline void load_weights(const DecodeParams& p, int base, int lane,
                                     int32_t (&w)[kPlanRegs], int32_t (&raw)[kPlanRegs]) {
 #pragma unroll
-  for (int r = 0; r < kPlanRegs; ++r) raw[r] = p.lens[min(base + r * kWave + lane, p.batch - 1)];
+  for (int r = 0; r < kPlanRegs; ++r)
+    raw[r] = base + r * kWave < p.batch ? p.lens[min(base + r * kWave + lane, p.batch - 1)] : 0;
 #pragma unroll
   for (int r = 0; r < kPlanRegs; ++r)
     w[r] = (base + r * kWave + lane < p.batch) ? pair_weight(raw[r], p.mbps) : 0;
@@ -318,14 +319,16 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   si.s0 = slice_start_u(wave, si.geo);
   si.s1 = slice_start_u(wave + 1, si.geo);
 
-  // Request b holds positions [hkv*P_b, hkv*P_{b+1}) with P the weight prefix sum.
-  const int32_t u = si.s0 / p.hkv;
+  // Request b holds positions [hkv*P_b, hkv*P_{b+1}) with P the weight prefix
+  // sum: the first b with hkv * P_{b+1} > s0 (no division by hkv).
+  const int32_t s0 = si.s0;
   int32_t carry = 0;
   int32_t found_b = -1, found_p = 0, found_w = 1, found_len = 0;
   for (int base = 0; base < p.batch && found_b < 0; base += kChunk) {
     if (p.batch > kChunk) load_weights(p, base, lane, w, raw);
-    // The register (64 requests) holding position u, then the lane. With one
-    // register in use the first is it; otherwise every register's sum is
+    // The register (64 requests) holding position s0, then the lane. In a
+    // round of at most 64 requests the first register is it (every earlier
+    // round was passed by its total); otherwise every register's sum is
     // reduced at once (the independent reductions pipeline).
     int32_t wr = w[0], rawr = raw[0], rr = 0;
     if (p.batch - base > kWave) {
@@ -339,7 +342,7 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
       for (int r = 0; r < kPlanRegs; ++r) {
         const int32_t c = uniform(cs[r]);
         if (rr < 0) {
-          if (carry + c > u) rr = r; else carry += c;
+          if (p.hkv * (carry + c) > s0) rr = r; else carry += c;
         }
       }
       if (rr < 0) continue;  // past this round: carry holds its total
@@ -349,12 +352,9 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
           wr = w[r];
           rawr = raw[r];
         }
-    } else if (carry + wave_sum_i32(wr) <= u) {
-      carry += wave_sum_i32(wr);
-      continue;
     }
     const int32_t incl = wave_incl_scan_i32(wr);
-    const uint64_t hit = __ballot(carry + incl > u);
+    const uint64_t hit = __ballot(p.hkv * (carry + incl) > s0);
     const int first = __ffsll((unsigned long long)hit) - 1;
     found_b = base + rr * kWave + first;
     found_p = carry + __builtin_amdgcn_readlane(incl - wr, first);
