@@ -77,25 +77,37 @@ bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 ||
 // plan uses at most CUs x wavefronts per workgroup slices (one workgroup per
 // CU).
 constexpr int kMaxDevices = 64;
-std::atomic<int32_t> g_cu_count[kMaxDevices];
+// Per device ordinal: compute units in the low 16 bits, XCDs above (0: not
+// read yet).
+std::atomic<int32_t> g_device_shape[kMaxDevices];
 
-neo_status device_cu_count(int32_t* cus) {
+// Compute units and XCDs of the current device.
+neo_status device_shape(int32_t* cus, int32_t* xcds) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
   if (dev >= 0 && dev < kMaxDevices) {
-    const int32_t cached = g_cu_count[dev].load(std::memory_order_relaxed);
+    const int32_t cached = g_device_shape[dev].load(std::memory_order_relaxed);
     if (cached > 0) {
-      *cus = cached;
+      *cus = cached & 0xFFFF;
+      *xcds = cached >> 16;
       return NEO_OK;
     }
   }
-  int v = 0;
+  int v = 0, x = 0;
   e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess || v <= 0)
+  if (e != hipSuccess || v <= 0 || v > 0xFFFF)
     return set_error(NEO_ERR_HIP, "hipDeviceGetAttribute(cu count): %s", hipGetErrorString(e));
-  if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(v, std::memory_order_relaxed);
+  // An XCD count the runtime cannot give only turns the slice weights off.
+  if (hipDeviceGetAttribute(&x, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || x < 1 ||
+      x > 0x7FFF) {
+    (void)hipGetLastError();
+    x = 1;
+  }
+  if (dev >= 0 && dev < kMaxDevices)
+    g_device_shape[dev].store(v | (x << 16), std::memory_order_relaxed);
   *cus = v;
+  *xcds = x;
   return NEO_OK;
 }
 
@@ -182,8 +194,8 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   if (!aligned(workspace, 256))
     return set_error(NEO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
-  int32_t cus = 0;
-  st = device_cu_count(&cus);
+  int32_t cus = 0, xcds = 0;
+  st = device_shape(&cus, &xcds);
   if (st != NEO_OK) return st;
   const int32_t quantum = cus * neo::kWavesPerGroup;
   // Default: at most one slice per wave of one workgroup per CU (the policy
@@ -221,13 +233,14 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   p.max_slices = slices;
   p.min_tiles = min_tiles;
   p.slice_quantum = quantum;
+  p.xcd8 = xcds == 8;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (sched == neo::kStaged) {
     e = neo::launch_plan(seq_lens, batch, num_kv_heads, max_blocks_per_seq, slices, min_tiles,
-                         quantum, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
+                         quantum, p.xcd8, reinterpret_cast<neo::PlanHeader*>(ws + wl.hdr),
                          reinterpret_cast<neo::SliceStart*>(ws + wl.starts),
                          reinterpret_cast<int32_t*>(ws + wl.prefix), s);
     if (e != hipSuccess) return set_error(NEO_ERR_HIP, "plan launch: %s", hipGetErrorString(e));

@@ -149,9 +149,11 @@ __device__ inline float uniform_f32(float v) {
 __device__ inline SliceGeom make_uniform(SliceGeom g) {
   g.W = uniform(g.W);
   g.n = uniform(g.n);
+  g.weighted = uniform(g.weighted);
+  g.cn = uniform(g.cn);
   g.a = uniform(g.a);
   g.r = uniform(g.r);
-  g.inv_n = uniform_f32(g.inv_n);
+  g.r_over_cn = uniform_f32(g.r_over_cn);
   g.n_over_w = uniform_f32(g.n_over_w);
   return g;
 }
@@ -256,7 +258,7 @@ __device__ inline float sum_over_rows(float v) {
 // Slice from the plan kernel's output (staged launch).
 __device__ inline SliceInfo read_plan(const DecodeParams& p, int wave) {
   SliceInfo si;
-  si.geo = make_slice_geom(p.hdr->total, p.hdr->n_slices);
+  si.geo = make_slice_geom(p.hdr->total, p.hdr->n_slices, p.xcd8 != 0);
   if (wave >= si.geo.n) return si;
   const SliceStart a = p.starts[wave];
   si.s0 = a.pos;
@@ -314,7 +316,7 @@ __device__ inline SliceInfo plan_in_wave(const DecodeParams& p, int wave, int la
   }
   const int32_t W = uniform(total * p.hkv);
   si.geo = make_uniform(
-      make_slice_geom(W, slice_count(W, p.min_tiles, p.max_slices, p.slice_quantum)));
+      make_slice_geom(W, slice_count(W, p.min_tiles, p.max_slices, p.slice_quantum), p.xcd8 != 0));
   if (wave >= si.geo.n) return si;
   si.s0 = slice_start_u(wave, si.geo);
   si.s1 = slice_start_u(wave + 1, si.geo);

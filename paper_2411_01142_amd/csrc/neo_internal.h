@@ -43,42 +43,72 @@ __host__ __device__ inline int32_t pair_cost(int32_t nb) {
                                : (nb >= kShortPairBlocks ? kPairCost : kPairCostShort);
 }
 
-// Slice geometry of the weighted line: W positions cut into n slices, slice s
-// owning [floor(sW/n), floor((s+1)W/n)). Evaluated without 64-bit division,
-// which the GPU has no instruction for (the software sequence would run at
-// every pair transition and merge): with W = a n + r, floor(sW/n) =
-// s a + floor(s r / n), where s r < n^2 <= 2^24 is exact in fp32; the fp32
-// quotient is within one of that floor and one exact integer step corrects it.
+// Slice geometry of the weighted line: W positions cut into n slices. Slice s
+// owns [floor(C(s) W / C(n)), floor(C(s+1) W / C(n))), C(s) being the units of
+// the slices before s: one per slice, or, on a part with eight XCDs and slices
+// of at least kXcdWeightMinTiles positions, kXcdEvenUnits for a slice on an
+// even-numbered XCD and kXcdOddUnits for one on an odd-numbered XCD.
+// Workgroups are dispatched round-robin over the XCDs in index order (the
+// hardware XCC id read back was workgroup index mod 8 in every run), and
+// workgroup w holds slices 4w .. 4w+3, so slice s runs on XCD (s / 4) mod 8.
+// Measured on MI355X: waves on the odd-numbered XCDs stream 5-8 % slower, so
+// with equal slices they end last; 34 : 30 units gain 0.9 points on a
+// 256-request lognormal mix and 1.2 on a 70B layer, while on short slices
+// (43 tiles, batch 64) any weighting measured 0.7-1.0 points slower.
+//
+// Evaluated without 64-bit division, which the GPU has no instruction for
+// (the software sequence would run at every pair transition and merge): with
+// W = a C(n) + r, floor(C(s) W / C(n)) = C(s) a + floor(C(s) r / C(n)); the
+// fp32 estimate of the last term is within one of it (it is below 2^17) and
+// one exact integer step corrects it.
+constexpr int32_t kXcdEvenUnits = 34;
+constexpr int32_t kXcdOddUnits = 30;
+constexpr int32_t kXcdWeightMinTiles = 128;
+constexpr int32_t kXcdPeriodUnits = 4 * (kXcdEvenUnits + kXcdOddUnits);  // 8 slices
 struct SliceGeom {
-  int32_t W, n;     // positions and slices, 0 < n <= min(W, NEO_MAX_SLICES) (n = 0: no slices)
-  int32_t a, r;     // W = a n + r
-  float inv_n;      // 1 / n
-  float n_over_w;   // n / W
+  int32_t W, n;      // positions and slices, 0 < n <= min(W, NEO_MAX_SLICES) (n = 0: no slices)
+  int32_t weighted;  // 1: slices weighed by XCD
+  int32_t cn;        // C(n)
+  int32_t a, r;      // W = a C(n) + r
+  float r_over_cn;   // r / C(n)
+  float n_over_w;    // n / W
 };
-static_assert((int64_t)NEO_MAX_SLICES * NEO_MAX_SLICES <= (int64_t)1 << 24,
-              "s r must be exact in fp32");
+static_assert((int64_t)(NEO_MAX_SLICES / 8) * kXcdPeriodUnits < ((int64_t)1 << 24),
+              "C(s) must be exact in fp32");
 
-__host__ __device__ inline SliceGeom make_slice_geom(int32_t W, int32_t n) {
+// xcd8: the device has eight XCDs.
+__host__ __device__ inline SliceGeom make_slice_geom(int32_t W, int32_t n, bool xcd8) {
   SliceGeom g;
   g.W = W;
   g.n = n;
-  g.a = n > 0 ? W / n : 0;
-  g.r = W - g.a * n;
-  g.inv_n = n > 0 ? 1.f / (float)n : 0.f;
+  g.weighted = xcd8 && n > 0 && n % 8 == 0 && W / kXcdWeightMinTiles >= n;
+  g.cn = g.weighted ? (n / 8) * kXcdPeriodUnits : n;
+  g.a = g.cn > 0 ? W / g.cn : 0;
+  g.r = W - g.a * g.cn;
+  g.r_over_cn = g.cn > 0 ? (float)g.r / (float)g.cn : 0.f;
   g.n_over_w = W > 0 ? (float)n / (float)W : 0.f;
   return g;
 }
-// floor(sW/n), for 0 <= s <= n.
+// C(s), for 0 <= s <= n.
+__host__ __device__ inline int32_t slice_units(int32_t s, const SliceGeom& g) {
+  if (!g.weighted) return s;
+  const int32_t k = s & 7;
+  return (s >> 3) * kXcdPeriodUnits +
+         (k < 4 ? k * kXcdEvenUnits : 4 * kXcdEvenUnits + (k - 4) * kXcdOddUnits);
+}
+// First position of slice s, for 0 <= s <= n.
 __host__ __device__ inline int32_t slice_start(int32_t s, const SliceGeom& g) {
-  const int32_t sr = s * g.r;
-  int32_t q = (int32_t)((float)sr * g.inv_n);
-  const int32_t t = sr - q * g.n;
-  q += t < 0 ? -1 : (t >= g.n ? 1 : 0);
-  return s * g.a + q;
+  const int32_t c = slice_units(s, g);
+  int32_t q = (int32_t)((float)c * g.r_over_cn);
+  const int64_t t = (int64_t)c * g.r - (int64_t)q * g.cn;
+  q += t < 0 ? -1 : (t >= g.cn ? 1 : 0);
+  return c * g.a + q;
 }
 // The slice holding position x, 0 <= x < W: the largest s with
-// slice_start(s) <= x, i.e. ceil((x+1) n / W) - 1. The fp32 estimate of
-// (x+1) n / W is within 2^-10 of it, so its floor is off by at most one.
+// slice_start(s) <= x. For equal slices that is ceil((x+1) n / W) - 1, and the
+// fp32 estimate of (x+1) n / W is within 2^-10 of it; XCD weights move a
+// boundary by at most 4 (34 - 30) / 64 = 0.25 slices. Either way the estimate's
+// floor is off by at most one.
 __host__ __device__ inline int32_t slice_of(int32_t x, const SliceGeom& g) {
   int32_t s = (int32_t)(((float)x + 1.f) * g.n_over_w);
   s = s < g.n - 1 ? s : g.n - 1;
@@ -164,13 +194,14 @@ struct DecodeParams {
   int32_t batch, hq, hkv, mbps, num_blocks;
   int32_t max_slices, min_tiles;  // min_tiles == 0: the default slice policy
   int32_t slice_quantum;          // compute units x wavefronts per workgroup
+  int32_t xcd8;                   // the device has eight XCDs (slice weights)
   float scale_log2;           // scale * log2(e)
 };
 
 // Launchers (each returns the hipError_t of its launch).
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
-                       int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* hdr,
-                       SliceStart* starts, int32_t* prefix, hipStream_t stream);
+                       int32_t max_slices, int32_t min_tiles, int32_t quantum, int32_t xcd8,
+                       PlanHeader* hdr, SliceStart* starts, int32_t* prefix, hipStream_t stream);
 hipError_t launch_decode_valu(const DecodeParams& p, int32_t group, Schedule sched,
                               int32_t grid, hipStream_t stream);
 hipError_t launch_decode_mfma(const DecodeParams& p, int32_t group, Schedule sched,

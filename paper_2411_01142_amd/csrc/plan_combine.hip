@@ -21,7 +21,8 @@ constexpr int kPlanLdsBatch = 8192;
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t* __restrict__ lens, int32_t batch, int32_t hkv, int32_t mbps,
-    int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* __restrict__ hdr,
+    int32_t max_slices, int32_t min_tiles, int32_t quantum, int32_t xcd8,
+    PlanHeader* __restrict__ hdr,
     SliceStart* __restrict__ starts, int32_t* __restrict__ prefix) {
   __shared__ int32_t sums[kPlanThreads];
   __shared__ int32_t sprefix[kPlanLdsBatch + 1];
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   const int32_t* pre = in_lds ? sprefix : prefix;
 
   const int32_t n = slice_count(total, min_tiles, max_slices, quantum);
-  const SliceGeom geo = make_slice_geom(total, n);
+  const SliceGeom geo = make_slice_geom(total, n, xcd8 != 0);
   for (int s = tid; s <= n; s += kPlanThreads) {
     SliceStart st;
     st.pad[0] = st.pad[1] = st.pad[2] = 0;
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void combine_kernel(DecodeP
   const int32_t cost = pair_cost(a.nb);
   if (a.x <= cost) return;                      // no tile of the pair before the boundary
   const int32_t first_tile = a.pos - a.x + cost;
-  const SliceGeom geo = make_slice_geom(W, n);
+  const SliceGeom geo = make_slice_geom(W, n, p.xcd8 != 0);
   const int32_t prev_start = slice_start(s - 1, geo);
   if (first_tile < prev_start) return;          // an earlier boundary cuts it first
   const int32_t c1 = slice_of(first_tile + a.nb - 1, geo);
@@ -207,10 +208,10 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_plan(const int32_t* lens, int32_t batch, int32_t hkv, int32_t mbps,
-                       int32_t max_slices, int32_t min_tiles, int32_t quantum, PlanHeader* hdr,
-                       SliceStart* starts, int32_t* prefix, hipStream_t stream) {
+                       int32_t max_slices, int32_t min_tiles, int32_t quantum, int32_t xcd8,
+                       PlanHeader* hdr, SliceStart* starts, int32_t* prefix, hipStream_t stream) {
   plan_kernel<<<1, kPlanThreads, 0, stream>>>(lens, batch, hkv, mbps, max_slices, min_tiles,
-                                              quantum, hdr, starts, prefix);
+                                              quantum, xcd8, hdr, starts, prefix);
   return hipGetLastError();
 }
 

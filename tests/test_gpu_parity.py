@@ -303,6 +303,23 @@ def test_group_merge_mixes_contributor_counts(variant):
         assert np.array_equal(a, b), f"fused != two_kernel at {slices} slices"
 
 
+@pytest.mark.parametrize("variant", ["valu", "mfma"])
+def test_xcd_weighted_slices(variant):
+    # On a part with eight XCDs, slice counts that are multiples of 8 with at
+    # least 128 positions per slice weigh the slices by XCD (34 : 30 units):
+    # 8 and 16 slices here (~300 and ~150 positions), 24 slices stay equal
+    # (~100). Every schedule must match the oracle and each other bit for bit.
+    lens = [3000, 40, 5000, 16, 2500, 7000, 1, 1257]
+    case = W.build_case(lens, 8, 2, 128, 16, seed=37)
+    ref = oracle.decode_attention(case)
+    for slices in (8, 16, 24):
+        a = run(case, variant=variant, schedule="fused", max_slices=slices)
+        b = run(case, variant=variant, schedule="two_kernel", max_slices=slices)
+        c = run(case, variant=variant, schedule="staged", max_slices=slices)
+        assert_parity(a, ref, f"xcd weights {variant} slices={slices}")
+        assert np.array_equal(a, b) and np.array_equal(a, c), f"schedules differ at {slices}"
+
+
 def test_batch_beyond_one_plan_round():
     # More than 1024 requests: the in-kernel plan reads seq_lens in rounds of
     # 1024 requests; slices must start in the right request in every round

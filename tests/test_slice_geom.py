@@ -2,7 +2,8 @@
 no 64-bit division) against its exact integer definition, on the host.
 
 The same header the kernels include is compiled host-only with hipcc; the
-program checks every slice boundary of several thousand (W, n) pairs."""
+program checks every slice boundary of several thousand (W, n) pairs, with and
+without the per-XCD slice weights."""
 import os
 import subprocess
 
