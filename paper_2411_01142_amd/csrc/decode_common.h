@@ -5,13 +5,14 @@
 //
 // Work is balanced on a weighted line: each (request, kv head) pair with nb > 0
 // blocks occupies nb + pair_cost(nb) positions, its startup cost (q, block
-// ids, pipeline fill, result write) followed by one position per block tile. With W positions in
-// all and n slices, slice s owns [floor(sW/n), floor((s+1)W/n)) and processes
-// the tiles whose positions fall there. A pair whose tiles cross a slice
-// boundary is "cut": every slice holding some of its tiles writes a partial
-// output normalised over its share plus the log-sum-exp of its scores, and the
-// pair is aggregated afterwards (the block-granular split and per-request
-// aggregation of Sec. 4 of the paper).
+// ids, pipeline fill, result write) followed by one position per block tile.
+// The W positions are cut into n contiguous slices (equal ones, or, for long
+// slices on an eight-XCD part, weighted by the XCD each runs on: SliceGeom),
+// and each slice processes the tiles whose positions fall in it. A pair
+// whose tiles cross a slice boundary is "cut": every slice holding some of
+// its tiles writes a partial output normalised over its share plus the
+// log-sum-exp of its scores, and the pair is aggregated afterwards (the
+// block-granular split and per-request aggregation of Sec. 4 of the paper).
 #pragma once
 
 #include <math.h>
