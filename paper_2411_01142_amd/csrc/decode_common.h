@@ -737,11 +737,16 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // before the segment ends (late enough that the next slice has usually
     // finished its share, early enough that the read's latency hides behind
     // the remaining tiles) and only looked at after the tiles.
+    // The slices holding the pair's first and last tiles, if the pair is cut
+    // (computed here, where their latency hides behind the first tile's
+    // round trip; after the tiles it delayed every cut segment's result).
+    const bool cut = j > 0 || jend < nb;
+    const int32_t c0 = cut ? slice_of_u(first_tile, si.geo) : 0;
+    const int32_t c1 = cut ? slice_of_u(first_tile + nb - 1, si.geo) : 0;
     bool fast_cand = false;
     if constexpr (kMergeHere && F::kFastMerge)
       fast_cand = j == 0 && jend < nb &&
-                  (!group_merge || wave + 1 == first_slice + kWavesPerGroup) &&
-                  slice_of_u(first_tile + nb - 1, si.geo) == wave + 1;
+                  (!group_merge || wave + 1 == first_slice + kWavesPerGroup) && c1 == wave + 1;
     const int32_t check_at = fast_cand ? max(j, jend - kMergeCheckAhead) : -1;
     int32_t seen = 0;
     for (int32_t jj = j; jj < jend; jj += PF + 1) {
@@ -772,12 +777,9 @@ __device__ inline void decode_driver(const DecodeParams& p) {
         F::merge_write(st, p.part_o + (size_t)slot * G * kHeadDim, p.part_lse + slot * G,
                        p.out + ((size_t)b * p.hq + g * G) * kHeadDim, lane);
       }
-    } else if (group_merge && slice_of_u(first_tile, si.geo) >= first_slice &&
-               slice_of_u(first_tile + nb - 1, si.geo) < first_slice + kWavesPerGroup) {
+    } else if (group_merge && c0 >= first_slice && c1 < first_slice + kWavesPerGroup) {
       if constexpr (kMergeHere) {
         // Every contributor is a wave of this workgroup: merge through LDS.
-        const int32_t c0 = slice_of_u(first_tile, si.geo);
-        const int32_t c1 = slice_of_u(first_tile + nb - 1, si.geo);
         const int32_t slot0 = 2 * first_slice;
         constexpr int kLdsMergeHeads = GroupMerge<G>::kHeadsPerPass;
         const int ls = partial_slot(wave, si.s0, first_tile) - slot0;
@@ -813,8 +815,6 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       F::template write<kMergeHere>(st, p.part_o + (size_t)slot * G * kHeadDim,
                                 p.part_lse + slot * G, lane);
       if (kMergeHere) {
-        const int32_t c0 = slice_of_u(first_tile, si.geo);
-        const int32_t c1 = slice_of_u(first_tile + nb - 1, si.geo);
         if (arrive_last(p, c0, c1, lane)) {
           const Pending rec{b, g, first_tile, c0, c1};
           if (npend == 0) pend0 = rec; else pend1 = rec;

@@ -109,12 +109,14 @@ __host__ __device__ inline int32_t slice_start(int32_t s, const SliceGeom& g) {
 // fp32 estimate of (x+1) n / W is within 2^-10 of it; XCD weights move a
 // boundary by at most 4 (34 - 30) / 64 = 0.25 slices. Either way the estimate's
 // floor is off by at most one.
+// Branch-free (both neighbours' starts are computed): the kernels call it
+// with wave-uniform x, but in vector registers, where a branch costs masking.
 __host__ __device__ inline int32_t slice_of(int32_t x, const SliceGeom& g) {
   int32_t s = (int32_t)(((float)x + 1.f) * g.n_over_w);
   s = s < g.n - 1 ? s : g.n - 1;
-  if (slice_start(s, g) > x) --s;
-  else if (s + 1 < g.n && slice_start(s + 1, g) <= x) ++s;
-  return s;
+  const bool down = slice_start(s, g) > x;
+  const bool up = s + 1 < g.n && slice_start(s + 1, g) <= x;
+  return down ? s - 1 : (up ? s + 1 : s);
 }
 
 struct alignas(16) PlanHeader {
