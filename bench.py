@@ -126,6 +126,8 @@ class HipEvents:
 def cpu_baseline(case, min_seconds: float = 10.0):
     """The fp64 oracle on the host cores over the whole batch, repeated until
     ``min_seconds`` have passed; same units as the GPU figure."""
+    import numpy as np
+
     import oracle
     threads = oracle.max_threads()
     passes, t0 = 0, time.perf_counter()
@@ -136,10 +138,27 @@ def cpu_baseline(case, min_seconds: float = 10.0):
         if el >= min_seconds:
             break
     gbs = case.algorithmic_bytes() * passes / el / 1e9
+    # One thread over the first requests (a bounded sample: ~3 s).
+    nreq = min(case.batch, 8)
+    L = np.maximum(case.seq_lens[:nreq].astype(np.int64), 0)
+    sample_bytes = (int(L.sum()) * case.num_kv_heads * case.head_dim * 4 +
+                    nreq * case.num_q_heads * case.head_dim * 6 +
+                    4 * int(((L + case.block_size - 1) // case.block_size).sum()) + 4 * nreq)
+    passes1, t1 = 0, time.perf_counter()
+    while True:
+        oracle.decode_attention(case, rows=(0, nreq * case.num_q_heads), threads=1)
+        passes1 += 1
+        el1 = time.perf_counter() - t1
+        if el1 >= min(3.0, min_seconds):
+            break
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"full batch ({case.batch} requests x {case.num_q_heads} heads), "
                       f"{passes} pass(es) in {el:.1f} s, fp64 naive softmax, OpenMP",
-            "tokens_per_s_per_layer": round(case.batch * passes / el, 2)}
+            "tokens_per_s_per_layer": round(case.batch * passes / el, 2),
+            "single_thread": {"value": round(sample_bytes * passes1 / el1 / 1e9, 4),
+                              "unit": "GB/s", "cores": 1,
+                              "sample": f"first {nreq} requests, {passes1} pass(es) in "
+                                        f"{el1:.1f} s"}}
 
 
 def copy_calibration(nbytes: int = 2 ** 30, reps: int = 5):
