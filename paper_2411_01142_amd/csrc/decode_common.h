@@ -729,6 +729,13 @@ __device__ inline void decode_driver(const DecodeParams& p) {
       pf_L = Lq;
     }
 
+    // The slices holding the pair's first and last tiles, if the pair is cut
+    // (computed here, where their latency hides behind the first tile's
+    // round trip; after the tiles it delayed every cut segment's result).
+    const bool cut = j > 0 || jend < nb;
+    const int32_t c0 = cut ? slice_of_u(first_tile, si.geo) : 0;
+    const int32_t c1 = cut ? slice_of_u(first_tile + nb - 1, si.geo) : 0;
+
     // Fused launch, last pair of this slice cut with exactly one later slice
     // (the next one), which handles its share of the pair first: if it has
     // already arrived, this slice will be the last, so it merges straight
@@ -737,12 +744,6 @@ __device__ inline void decode_driver(const DecodeParams& p) {
     // before the segment ends (late enough that the next slice has usually
     // finished its share, early enough that the read's latency hides behind
     // the remaining tiles) and only looked at after the tiles.
-    // The slices holding the pair's first and last tiles, if the pair is cut
-    // (computed here, where their latency hides behind the first tile's
-    // round trip; after the tiles it delayed every cut segment's result).
-    const bool cut = j > 0 || jend < nb;
-    const int32_t c0 = cut ? slice_of_u(first_tile, si.geo) : 0;
-    const int32_t c1 = cut ? slice_of_u(first_tile + nb - 1, si.geo) : 0;
     bool fast_cand = false;
     if constexpr (kMergeHere && F::kFastMerge)
       fast_cand = j == 0 && jend < nb &&
