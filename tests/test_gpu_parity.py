@@ -361,7 +361,7 @@ def random_case(i):
                         poison=bool(i % 2)), slices
 
 
-@pytest.mark.parametrize("i", range(40))
+@pytest.mark.parametrize("i", range(120))
 def test_random_shapes(i):
     # Seeded random batches: lengths from empty to 3000 tokens (short, long,
     # mixed and exact block multiples), groups 1-16, 1-8 kv heads, default or
