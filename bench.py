@@ -55,7 +55,11 @@ def pct(values, qs):
 
 
 def kernel_source_sha(variant: str) -> str:
+    from paper_2411_01142_amd import _build
     h = hashlib.sha256()
+    # The source's own compiler flags (none for most) are part of the kernel.
+    h.update(" ".join(_build.HIPCC_SOURCE_FLAGS.get(f"decode_{variant.split('_')[0]}.hip",
+                                                    [])).encode())
     for name in KERNEL_SOURCES:
         if name.startswith("decode_") and name != "decode_common.h" and \
                 name != f"decode_{variant.split('_')[0]}.hip":

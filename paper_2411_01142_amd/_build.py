@@ -27,6 +27,13 @@ HIPCC_FLAGS = [
     # No packed fp32 arithmetic in device code.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
+# Per-source additions. The decode kernel's first four arguments (five dwords:
+# lengths pointer, batch, kv heads, table stride) arrive preloaded in SGPRs,
+# so each wave's first length read goes out without waiting for a
+# kernel-argument load.
+HIPCC_SOURCE_FLAGS = {
+    "decode_mfma.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=4"],
+}
 
 
 def hipcc() -> str:
@@ -48,7 +55,8 @@ def _compile(src: str) -> str:
     if src in HOST_SOURCES:
         cmd = [cxx(), *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     else:
-        cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc(), *HIPCC_FLAGS, *HIPCC_SOURCE_FLAGS.get(src, []), "-c",
+               os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{res.stdout}\n{res.stderr}")

@@ -194,7 +194,16 @@ struct MfmaFamily {
 };
 
 template <int G, Schedule kSched>
-__global__ __launch_bounds__(kWave * kWavesPerGroup, 2) void decode_mfma_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kWave * kWavesPerGroup, 2) void decode_mfma_kernel(
+    const int32_t* __restrict__ lens, int32_t batch, int32_t hkv, int32_t mbps, DecodeParams p) {
+  // The first step of every wave reads the request lengths: the arguments it
+  // needs for that come first and separately, so that they can arrive in
+  // registers with the wave (kernel-argument preload) instead of one scalar
+  // load round trip later.
+  p.lens = lens;
+  p.batch = batch;
+  p.hkv = hkv;
+  p.mbps = mbps;
   // One tile in flight ahead of the one being computed: with 4 waves on every
   // CU that keeps HBM saturated; deeper prefetch measured equal or slower
   // (more requests in flight lower the HBM efficiency).
@@ -205,9 +214,9 @@ template <int G>
 hipError_t launch_g(const DecodeParams& p, Schedule sched, int32_t grid, hipStream_t stream) {
   const dim3 block(kWave * kWavesPerGroup);
   switch (sched) {
-    case kStaged: decode_mfma_kernel<G, kStaged><<<grid, block, 0, stream>>>(p); break;
-    case kFused: decode_mfma_kernel<G, kFused><<<grid, block, 0, stream>>>(p); break;
-    case kTwoKernel: decode_mfma_kernel<G, kTwoKernel><<<grid, block, 0, stream>>>(p); break;
+    case kStaged: decode_mfma_kernel<G, kStaged><<<grid, block, 0, stream>>>(p.lens, p.batch, p.hkv, p.mbps, p); break;
+    case kFused: decode_mfma_kernel<G, kFused><<<grid, block, 0, stream>>>(p.lens, p.batch, p.hkv, p.mbps, p); break;
+    case kTwoKernel: decode_mfma_kernel<G, kTwoKernel><<<grid, block, 0, stream>>>(p.lens, p.batch, p.hkv, p.mbps, p); break;
   }
   return hipGetLastError();
 }
