@@ -2,13 +2,17 @@
 
 One step = one call of the whole path (plan, decode, combine kernels) over one
 batch: every request of the batch decodes one token through one attention
-layer. The default workload is the Llama-3-8B layer shape (32 q heads, 8 kv
-heads, head_dim 128, block 16), batch 64, lengths uniform in [512, 2048],
-shuffled physical blocks, bf16 q/K/V ~ N(0,1) (synthetic, seeded).
+layer. The default workload is the largest one-GPU configuration, the
+Llama-3.1-70B layer shape (64 q heads, 8 kv heads, head_dim 128, block 16),
+batch 512, lengths uniform in [256, 4096] (the paper's 70B setting, Sec. 5.1,
+with code-generation-like lengths), shuffled physical blocks, bf16 q/K/V
+~ N(0,1) (synthetic, seeded): 4.6 GB of KV per call. `--config 1..5` picks
+the other workloads.
 
-Inputs are resident in HBM before timing. The KV cache is replicated enough
-times that consecutive steps never find their data in the 256 MB Infinity
-Cache (each replica holds identical values). Prints one JSON line.
+Inputs are resident in HBM before timing. The KV cache is replicated (at least
+two copies, rotated, and at least 4x the 256 MB Infinity Cache in total) so that
+consecutive steps never find their data in that cache; a third pass also
+times each call alone after a 1 GiB write. Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config N] [--variant auto|valu|mfma]
     python bench.py --copy-calibration     # plain copy of known size, for rocprofv3 --pmc
@@ -306,36 +310,56 @@ def bench_kv_op(args, torch, neo, W):
 
 
 def bench_read_ceiling(args, torch, neo):
-    """The device's streaming-read rate over 4 GiB (the practical ceiling of an
-    HBM-bound kernel that reads its data once), nontemporal and plain loads."""
+    """The device's read rate over 4 GiB with two probes: the strided probe
+    (every thread 16 bytes, 8 loads in flight, the whole grid sweeping the
+    buffer), nontemporal and plain loads; and the tile probe, the decode
+    kernel's own pattern without its arithmetic (contiguous 8 KiB steps per
+    wave through 4 KiB buffer resources, nontemporal), over a sweep of waves per
+    compute unit and steps in flight. The best median is the measured read
+    ceiling."""
     nbytes = 4 << 30
     src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
     sink = torch.empty(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
     hip = HipEvents()
     sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    rates = {}
-    for nt in (True, False):
+    reps = max(args.steps // 10, 5)
+
+    def rate(fn):
         for _ in range(2):
-            neo.read_probe(src, sink, nontemporal=nt)
+            fn()
         ms = []
-        for _ in range(max(args.steps // 10, 5)):
+        for _ in range(reps):
             a, b = hip.create(), hip.create()
             hip.record(a, sh)
-            neo.read_probe(src, sink, nontemporal=nt)
+            fn()
             hip.record(b, sh)
             torch.cuda.synchronize()
             ms.append(hip.elapsed_ms(a, b))
             hip.destroy(a)
             hip.destroy(b)
-        rates["nontemporal" if nt else "plain"] = [round(nbytes / (m * 1e-3) / 1e9, 1) for m in ms]
-    best = max(max(v) for v in rates.values())
+        return [round(nbytes / (m * 1e-3) / 1e9, 1) for m in ms]
+    rates = {}
+    for nt in (True, False):
+        rates["strided_" + ("nontemporal" if nt else "plain")] = rate(
+            lambda: neo.read_probe(src, sink, nontemporal=nt))
+    # Waves per CU that the kernel's registers allow at each depth (51, 107,
+    # 144 and 175 VGPRs: 8, 4, 3 and 2 waves per SIMD).
+    fits = {1: (4, 8, 12, 16), 2: (4, 8, 12, 16), 3: (4, 8, 12), 4: (4, 8)}
+    for depth, wpcs in fits.items():
+        for wpc in wpcs:
+            rates[f"tiles_w{wpc}_d{depth}"] = rate(
+                lambda: neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth))
+            log(f"[bench] tile probe {wpc} waves/CU depth {depth}: "
+                f"{pct(rates[f'tiles_w{wpc}_d{depth}'], (50,))[0]} GB/s")
     med = {k: pct(v, (50,))[0] for k, v in rates.items()}
+    best_key = max(med, key=med.get)
     print(json.dumps({
-        "metric": "device streaming-read rate (read ceiling for HBM-bound kernels)",
-        "value": med["nontemporal"], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
-        "bytes": nbytes, "median_gbs": med, "best_gbs": best, "runs_gbs": rates,
-        "roofline": {"bound": "hbm", "achieved": med["nontemporal"], "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(med["nontemporal"] / PEAK_HBM_GBS, 4)},
+        "metric": "device read rate (measured read ceiling for HBM-bound kernels)",
+        "value": med[best_key], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+        "bytes": nbytes, "best_pattern": best_key,
+        "decode_pattern_gbs": med["tiles_w4_d1"], "median_gbs": med, "runs_gbs": rates,
+        "roofline": {"bound": "hbm", "achieved": med[best_key], "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(med[best_key] / PEAK_HBM_GBS, 4)},
     }), flush=True)
     return 0
 
@@ -616,7 +640,9 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-flush-pass", action="store_true",
+                    help="skip the per-call pass with a 1 GiB write before each call")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--variant", default="auto", choices=["auto", "valu", "mfma"])
     ap.add_argument("--schedule", default="auto",
@@ -671,7 +697,9 @@ def main(argv=None):
     workload_key = W.CONFIGS[args.config]["name"]
     q, k, v, bt, sl = case.to_torch("cuda")
     kv_bytes = k.numel() * 2 + v.numel() * 2
-    nrep = max(1, math.ceil(4 * MALL_BYTES / kv_bytes))
+    # At least two copies of the cache, rotated, and at least 4x the Infinity
+    # Cache in total: no step finds the tiles of the step before it there.
+    nrep = max(2, math.ceil(4 * MALL_BYTES / kv_bytes))
     reps = [(k, v)] + [(k.clone(), v.clone()) for _ in range(nrep - 1)]
     out = torch.empty((case.batch, case.num_q_heads, case.head_dim), dtype=torch.float32,
                       device="cuda")
@@ -722,6 +750,19 @@ def main(argv=None):
         step(args.warmup + args.steps + i, ev[i])
     torch.cuda.synchronize()
     decode_ms = [hip.elapsed_ms(a, b) for a, b in ev]
+
+    # Third pass, one call at a time: a 1 GiB write between calls (outside the
+    # events) evicts the Infinity Cache, so each call starts with none of its
+    # cache lines there; events right around the decode kernel.
+    flushed_ms = []
+    if not args.no_flush_pass:
+        scratch = torch.empty(2 ** 30 // 4, dtype=torch.float32, device="cuda")
+        for i in range(args.steps):
+            scratch.fill_(float(i))
+            step(2 * args.steps + args.warmup + i, ev[i])
+        torch.cuda.synchronize()
+        flushed_ms = [hip.elapsed_ms(a, b) for a, b in ev]
+        del scratch
     for a, b in ev + [region]:
         hip.destroy(a)
         hip.destroy(b)
@@ -778,8 +819,20 @@ def main(argv=None):
             "kernel_ms_event_pair": round(dec_ms, 5),
             # Per-call spread of the event pairs around the decode kernel.
             "kernel_ms_event_pair_p10_p50_p90": [round(x, 5) for x in pct(decode_ms, (10, 50, 90))],
+            # The same with the Infinity Cache evicted (1 GiB written) before each call.
+            "kernel_ms_flushed_p10_p50_p90": ([round(x, 5) for x in pct(flushed_ms, (10, 50, 90))]
+                                              if flushed_ms else None),
+            "achieved_flushed_median": (round(alg_bytes / (pct(flushed_ms, (50,))[0] * 1e-3)
+                                              / 1e9, 2) if flushed_ms else None),
             "gpu_ms_per_step": round(region_ms, 5),
             "algorithmic_bytes_per_launch": alg_bytes,
+            # Where `traffic` and the two counter rates below come from: not this run
+            # but a separate rocprofv3 --pmc run of the same command on the same kernel
+            # sources (FETCH_SIZE, then WRITE_SIZE, one counter per run), scaled by what
+            # each counter reads for a plain 1 GiB copy.
+            "traffic_source": (f"rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, separate profiled run: "
+                               f"profiles/counters__decode_{resolved}_{schedule}__{workload_key}.md"
+                               if traffic else None),
             # HBM bytes the counters saw (FETCH + WRITE, copy-calibrated) over the same
             # kernel time, beside the algorithmic rate above.
             "achieved_traffic_gbs": (round(traffic / (kernel_ms * 1e-3) / 1e9, 2)

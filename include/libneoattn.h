@@ -47,8 +47,14 @@
  * Block ids outside [0, num_blocks) are clamped to a valid block (no fault, wrong
  * result); seq_lens above max_blocks_per_seq * block_size are clamped to it and
  * negative ones read as 0. neo_debug_validate() reports both.
- * Concurrency: stateless apart from the thread-local error text. Calls that may
- * overlap on the device need distinct workspaces.
+ * State: the library keeps no state between calls apart from the thread-local
+ * error text and a per-device cache of the compute-unit and XCD counts. The
+ * caller's decode workspace does carry state from one call to the next: the
+ * arrival counters of split requests, which every call leaves at zero. A new
+ * workspace must therefore be zero-filled once before its first use
+ * (neo_decode_workspace_init, or any fill that has completed on the stream of
+ * the first call); a workspace that was never zeroed gives wrong merges, not
+ * an error. Calls that may overlap on the device need distinct workspaces.
  */
 #ifndef LIBNEOATTN_H
 #define LIBNEOATTN_H
@@ -94,7 +100,13 @@ typedef enum {
  * starts, per-request tile offsets) and room for two partial outputs per slice
  * (group * head_dim fp32 values plus group log-sum-exps each), and the arrival
  * counters of split requests. Depends only on host scalars, so it can be
- * allocated ahead of time. Sized for NEO_MAX_SLICES.
+ * allocated ahead of time. Sized for NEO_MAX_SLICES, so it depends on the
+ * batch (one int32 per request plus a fixed part) and on the query group
+ * (num_q_heads / num_kv_heads), never on the lengths or the pool size: the
+ * arguments are (batch, num_q_heads, num_kv_heads, head_dim), and the value is
+ * align256(16) + align256(32 * (NEO_MAX_SLICES + 1)) + align256(4 * NEO_MAX_SLICES)
+ * + align256(4 * (batch + 1)) + align256(8 * NEO_MAX_SLICES * group)
+ * + align256(8 * NEO_MAX_SLICES * group * head_dim) bytes.
  *
  * The workspace must be zero-filled once before its first use
  * (neo_decode_workspace_init or any fill); every call leaves its counters at
@@ -103,7 +115,10 @@ typedef enum {
 neo_status neo_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                       int32_t head_dim, size_t* bytes_out);
 
-/* Zero-fill a workspace on `stream` with a fill kernel (no memset node). */
+/* Zero-fill a workspace on `stream` with a fill kernel (no memset node, so it
+ * may be captured in a HIP graph). Enqueued like any kernel: a decode call on
+ * another stream must wait for it. workspace_bytes: the bytes to clear (the
+ * whole workspace); the workspace must be 256-byte aligned. */
 neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
 /*
@@ -111,8 +126,18 @@ neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, vo
  * The first eleven arguments follow the problem statement in that order; the rest
  * are what a device pointer cannot carry: batch size, block-table row stride
  * (max_blocks_per_seq), pool size (num_blocks), the workspace and the stream.
- * Enqueues two kernels (decode, combine). Reads q, k_cache, v_cache,
- * block_table and seq_lens; writes out and the workspace.
+ * Enqueues one kernel: each wavefront plans its own slice of the batch from
+ * seq_lens, streams its tiles, and the last slice to finish a request that
+ * was split merges the partial outputs in the same kernel (the staged and
+ * two-kernel launches of neo_decode_attention_ex add a plan and a combine
+ * kernel). Reads q, k_cache, v_cache, block_table and seq_lens; writes out and
+ * the workspace.
+ * Workspace: at least neo_decode_workspace_bytes(batch, num_q_heads,
+ * num_kv_heads, head_dim) bytes, 256-byte aligned, zero-filled before its
+ * first use and then reused as is (each call leaves its arrival counters at
+ * zero); NEO_ERR_WORKSPACE when it is NULL or too small.
+ * Limits: batch * (max_blocks_per_seq + 3) * num_kv_heads below 2^31 and
+ * max_blocks_per_seq * block_size below 2^31 (NEO_ERR_INVALID_ARG otherwise).
  * batch == 0 is a no-op (pointers may then be NULL).
  */
 neo_status neo_decode_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -210,6 +235,21 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
 #define NEO_READ_PROBE_SINK_WORDS 16384
 neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, uint32_t* sink,
                           size_t sink_words, void* stream);
+
+/*
+ * Measurement aid, not part of attention: the read rate of the decode kernel's
+ * own access pattern without its arithmetic. `bytes` (a positive multiple of
+ * 8192) at `src` (device memory, 256-byte aligned) are cut into 8 KiB steps
+ * (two 4 KiB tiles, like the K and V tiles of one block), the steps into one
+ * contiguous range per wavefront; waves_per_cu (4, 8, 12 or 16) wavefronts per
+ * compute unit in workgroups of four, each with `depth` (1-4) steps in flight
+ * ahead of the one it consumes; 16-byte nontemporal buffer loads. Writes one
+ * word per wavefront (compute units * waves_per_cu words, at most 4096 on
+ * MI355X) to `sink`: the xor of every 32-bit word that wave read, so the xor
+ * of all of them is the xor of the buffer. One kernel on `stream`.
+ */
+neo_status neo_read_probe_tiles(const void* src, size_t bytes, int32_t waves_per_cu,
+                                int32_t depth, uint32_t* sink, size_t sink_words, void* stream);
 
 neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                               const int32_t* src_ids, const int32_t* dst_ids, int32_t n,

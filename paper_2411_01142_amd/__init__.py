@@ -29,7 +29,7 @@ __all__ = [
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
     "new_workspace", "kv_append", "copy_blocks", "cpu_decode_attention", "CPU_ISAS",
     "cpu_best_isa", "cpu_default_threads", "cpu_read_probe", "cpu_kv_append",
-    "read_probe", "READ_PROBE_SINK_WORDS",
+    "read_probe", "read_probe_tiles", "READ_PROBE_SINK_WORDS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -98,6 +98,8 @@ def load_library():
         lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
         lib.neo_read_probe.argtypes = [P, S, I, P, S, P]
         lib.neo_read_probe.restype = ctypes.c_int
+        lib.neo_read_probe_tiles.argtypes = [P, S, I, I, P, S, P]
+        lib.neo_read_probe_tiles.restype = ctypes.c_int
         lib.neo_kv_copy_blocks.restype = ctypes.c_int
         lib.neo_cpu_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I, I]
         lib.neo_cpu_decode_attention_ex.restype = ctypes.c_int
@@ -158,27 +160,45 @@ def _require(t, name, dtype, ndim):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _stream_handle(stream, device):
+def _stream_of(stream, device):
     torch = _torch()
-    if stream is None:
-        stream = torch.cuda.current_stream(device)
-    return ctypes.c_void_p(stream.cuda_stream)
+    return torch.cuda.current_stream(device) if stream is None else stream
+
+
+def _stream_handle(stream, device):
+    return ctypes.c_void_p(_stream_of(stream, device).cuda_stream)
 
 
 def new_workspace(batch: int, num_q_heads: int, num_kv_heads: int, device="cuda",
-                  head_dim: int = 128):
-    """A zero-filled workspace (uint8 GPU tensor) sized for these shapes."""
+                  head_dim: int = 128, *, stream=None):
+    """A workspace (uint8 GPU tensor) sized for these shapes, allocated for and
+    zero-filled on ``stream`` (default: the current stream), so the first
+    decode call on that stream sees it cleared."""
     torch = _torch()
-    return torch.zeros(workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim),
-                       dtype=torch.uint8, device=device)
+    device = torch.device(device)
+    if device.index is None:
+        device = torch.device("cuda", torch.cuda.current_device())
+    s = _stream_of(stream, device)
+    nbytes = workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim)
+    with torch.cuda.device(device), torch.cuda.stream(s):
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _check(load_library().neo_decode_workspace_init(ws.data_ptr(), nbytes,
+                                                        ctypes.c_void_p(s.cuda_stream)))
+    return ws
 
 
-def _workspace(nbytes: int, device, stream_handle):
+def _workspace(nbytes: int, device, stream):
+    """The cached workspace of (device, stream): allocated in that stream's
+    pool and cleared on that stream, so the kernels that use it are ordered
+    after the fill and a replaced buffer is reused only after them."""
     torch = _torch()
-    key = (device.index, stream_handle.value)
+    key = (device.index, stream.cuda_stream)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.device(device), torch.cuda.stream(stream):
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+            _check(load_library().neo_decode_workspace_init(
+                ws.data_ptr(), nbytes, ctypes.c_void_p(stream.cuda_stream)))
         _workspaces[key] = ws
     return ws
 
@@ -194,9 +214,10 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
     combine); ``max_slices`` caps
     the sequence slices of the plan (0 = library default, 1 = never split a
     request). ``workspace`` (a zero-filled uint8 GPU tensor of at least
-    ``workspace_bytes(...)``, see ``new_workspace``) is allocated and cached per
-    device and stream when omitted. Runs on ``stream`` (default: torch's
-    current stream) without synchronising.
+    ``workspace_bytes(...)``, see ``new_workspace``; the fill must be ordered
+    before this call's stream reaches the kernel) is allocated, cleared on
+    ``stream`` and cached per device and stream when omitted. Runs on
+    ``stream`` (default: torch's current stream) without synchronising.
     """
     torch = _torch()
     lib = load_library()
@@ -229,12 +250,13 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
         raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
     if schedule not in SCHEDULES:
         raise ValueError(f"schedule must be one of {sorted(SCHEDULES)}")
-    sh = _stream_handle(stream, device)
+    st = _stream_of(stream, device)
+    sh = ctypes.c_void_p(st.cuda_stream)
     if B == 0:
         return out
     need = workspace_bytes(B, Hq, Hkv, D)
     if workspace is None:
-        workspace = _workspace(need, device, sh)
+        workspace = _workspace(need, device, st)
     else:
         _require(workspace, "workspace", torch.uint8, 1)
     with torch.cuda.device(device):
@@ -371,6 +393,23 @@ def read_probe(src, sink, *, nontemporal: bool = True, stream=None):
         _check(lib.neo_read_probe(src.data_ptr(), src.numel() * src.element_size(),
                                   int(bool(nontemporal)), sink.data_ptr(),
                                   sink.numel() * sink.element_size() // 4, sh))
+
+
+def read_probe_tiles(src, sink, *, waves_per_cu: int = 4, depth: int = 1, stream=None):
+    """Read the GPU tensor ``src`` (its bytes, a multiple of 8192) once in the
+    decode kernel's pattern (contiguous 8 KiB steps per wave, ``waves_per_cu``
+    waves per compute unit, ``depth`` steps in flight) and write one xor word
+    per wave into ``sink`` (``READ_PROBE_SINK_WORDS`` 32-bit words suffice).
+    Runs on ``stream`` without synchronising."""
+    torch = _torch()
+    lib = load_library()
+    if not (src.is_cuda and sink.is_cuda) or not src.is_contiguous() or not sink.is_contiguous():
+        raise ValueError("src and sink must be contiguous GPU tensors")
+    sh = _stream_handle(stream, src.device)
+    with torch.cuda.device(src.device):
+        _check(lib.neo_read_probe_tiles(src.data_ptr(), src.numel() * src.element_size(),
+                                        int(waves_per_cu), int(depth), sink.data_ptr(),
+                                        sink.numel() * sink.element_size() // 4, sh))
 
 
 def cpu_best_isa() -> str:

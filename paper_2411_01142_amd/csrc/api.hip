@@ -179,7 +179,8 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                      max_blocks_per_seq, num_blocks);
   if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCostLong) * num_kv_heads >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG,
-                     "batch * (max_blocks_per_seq + 2) * num_kv_heads must stay below 2^31");
+                     "batch * (max_blocks_per_seq + %d) * num_kv_heads must stay below 2^31",
+                     neo::kPairCostLong);
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
@@ -405,6 +406,31 @@ neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, ui
                      NEO_READ_PROBE_SINK_WORDS);
   const hipError_t e = neo::launch_read_probe(src, bytes / 16, nontemporal != 0, sink,
                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "probe launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+neo_status neo_read_probe_tiles(const void* src, size_t bytes, int32_t waves_per_cu,
+                                int32_t depth, uint32_t* sink, size_t sink_words, void* stream) {
+  if (!src || !sink) return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (bytes == 0 || bytes % 8192 != 0)
+    return set_error(NEO_ERR_INVALID_ARG, "bytes (%zu) must be a positive multiple of 8192",
+                     bytes);
+  if (!aligned(src, 256)) return set_error(NEO_ERR_INVALID_ARG, "src must be 256-byte aligned");
+  if (waves_per_cu < 4 || waves_per_cu > 16 || waves_per_cu % 4 != 0)
+    return set_error(NEO_ERR_INVALID_ARG, "waves_per_cu %d must be 4, 8, 12 or 16",
+                     waves_per_cu);
+  if (depth < 1 || depth > 4)
+    return set_error(NEO_ERR_INVALID_ARG, "depth %d outside [1, 4]", depth);
+  int32_t cus = 0, xcds = 0;
+  neo_status st = device_shape(&cus, &xcds);
+  if (st != NEO_OK) return st;
+  const size_t waves = (size_t)cus * waves_per_cu;
+  if (sink_words < waves)
+    return set_error(NEO_ERR_INVALID_ARG, "sink holds %zu words, needs %zu", sink_words, waves);
+  const hipError_t e =
+      neo::launch_read_probe_tiles(src, bytes / 8192, (int32_t)(waves / neo::kWavesPerGroup),
+                                   depth, sink, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "probe launch: %s", hipGetErrorString(e));
   return ok();
 }

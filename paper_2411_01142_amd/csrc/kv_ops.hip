@@ -8,13 +8,12 @@
 //    kernel on the caller's stream, so it overlaps with attention running on
 //    another stream, and pinned host memory is read or written directly over
 //    the host link in 16-byte accesses.
+#include "decode_common.h"
 #include "kv_ops.h"
 #include "neo_internal.h"
 
 namespace neo {
 namespace {
-
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One workgroup of 128 threads per (request, kv head): thread d writes dim d
 // of the value row (a 2-byte store: V is dim-major, so the token's dims are
@@ -148,7 +147,67 @@ __global__ __launch_bounds__(256) void read_probe_kernel(const probe_u32x4* __re
   if ((threadIdx.x & 63) == 0) sink[tid >> 6] = x;
 }
 
+// The decode kernel's access pattern without its arithmetic: one wave per
+// contiguous range of 8 KiB steps (two 4 KiB tiles, each read through a buffer
+// resource covering exactly that tile, 16-byte nontemporal loads, 1 KiB per
+// instruction), kDepth steps in flight ahead of the one consumed; a step past
+// the wave's range gets resources of size 0 (its loads return zeros without
+// touching memory), so every step issues the same loads. Workgroups of four
+// waves. The wave's xor goes to sink[wave].
+template <int kDepth>
+__global__ __launch_bounds__(256) void read_probe_tiles_kernel(const uint16_t* __restrict__ src,
+                                                               int64_t nsteps,
+                                                               uint32_t* __restrict__ sink) {
+  constexpr int kStepElems = 2 * kTileElems;  // 8 KiB of bf16
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = (int64_t)blockIdx.x * kWavesPerGroup + uniform(threadIdx.x >> 6);
+  const int64_t nw = (int64_t)gridDim.x * kWavesPerGroup;
+  const int64_t s0 = nsteps * wave / nw, s1 = nsteps * (wave + 1) / nw;
+  u32x4_t buf[kDepth + 1][8];
+  auto issue = [&](u32x4_t(&b)[8], int64_t s) {
+    const bool valid = s < s1;
+    const uint16_t* base = src + (valid ? s : s0) * kStepElems;
+    const __amdgpu_buffer_rsrc_t ra = tile_rsrc(base, valid);
+    const __amdgpu_buffer_rsrc_t rb = tile_rsrc(base + kTileElems, valid);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      b[u] = tile_load16(ra, 16 * (kWave * u + lane));
+      b[4 + u] = tile_load16(rb, 16 * (kWave * u + lane));
+    }
+  };
+  u32x4_t acc = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < kDepth; ++i) issue(buf[i], s0 + i);
+  for (int64_t s = s0; s < s1; s += kDepth + 1) {
+#pragma unroll
+    for (int u = 0; u <= kDepth; ++u) {
+      const int64_t cur = s + u;
+      if (cur >= s1) break;
+      issue(buf[(u + kDepth) % (kDepth + 1)], cur + kDepth);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc ^= buf[u][k];
+    }
+  }
+  uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x ^= __shfl_xor(x, o);
+  if (lane == 0) sink[wave] = x;
+}
+
 }  // namespace
+
+hipError_t launch_read_probe_tiles(const void* src, size_t nsteps, int32_t workgroups,
+                                   int32_t depth, uint32_t* sink, hipStream_t stream) {
+  const uint16_t* s = static_cast<const uint16_t*>(src);
+  const int64_t n = (int64_t)nsteps;
+  switch (depth) {
+    case 1: read_probe_tiles_kernel<1><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
+    case 2: read_probe_tiles_kernel<2><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
+    case 3: read_probe_tiles_kernel<3><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
+    default: read_probe_tiles_kernel<4><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_read_probe(const void* src, size_t n16, bool nontemporal, uint32_t* sink,
                              hipStream_t stream) {

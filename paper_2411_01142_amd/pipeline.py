@@ -149,11 +149,12 @@ class AsymmetricPipeline:
     """Runs iterations of the two-sub-batch schedule over `layers`."""
 
     def __init__(self, layers: List[LayerWeights], gpu: GpuBatch, cpu: CpuBatch, *,
-                 cpu_threads: int = 0):
+                 cpu_threads: int = 0, cpu_isa: str = "auto"):
         torch = _torch()
         self.torch = torch
         self.layers, self.gpu, self.cpu = layers, gpu, cpu
         self.threads = cpu_threads or max(1, cpu_default_threads() - 1)  # one core launches
+        self.isa = cpu_isa
         L0 = layers[0]
         B1 = cpu.x.shape[0]
         self.ws = new_workspace(gpu.x.shape[0], L0.hq, L0.hkv)
@@ -162,7 +163,9 @@ class AsymmetricPipeline:
         self.v1_h = torch.empty((B1, L0.hkv, L0.d), dtype=torch.bfloat16, pin_memory=True)
         self.o1_h = torch.empty((B1, L0.hq, L0.d), dtype=torch.float32, pin_memory=True)
         self.pool = cf.ThreadPoolExecutor(max_workers=1)
-        self.cpu_out = []  # per layer batch-1 attention outputs (host), when recording
+        # Per layer, when recording: both sub-batches' attention inputs and
+        # outputs (q0, o0 on the GPU; q1, o1 in host memory).
+        self.records = []
 
     def _to_host(self, q, k, v):
         self.q1_h.copy_(q, non_blocking=True)
@@ -177,7 +180,7 @@ class AsymmetricPipeline:
         c = self.cpu
         cpu_kv_append(c.k[layer], c.v[layer], self.k1_h, self.v1_h, c.table, c.lens)
         cpu_decode_attention(self.q1_h, c.k[layer], c.v[layer], c.table, c.lens,
-                             out=self.o1_h, num_threads=self.threads)
+                             out=self.o1_h, num_threads=self.threads, isa=self.isa)
 
     def iteration(self, *, overlap=True, record=False):
         """One decoding iteration through every layer; returns (x0, x1)."""
@@ -201,7 +204,8 @@ class AsymmetricPipeline:
                 torch.cuda.synchronize()
                 self._cpu_job(l, ready)
             if record:
-                self.cpu_out.append(self.o1_h.clone())
+                self.records.append({"q0": q0.clone(), "o0": o0.clone(),
+                                     "q1": self.q1_h.clone(), "o1": self.o1_h.clone()})
             # GPU, batch-1: output back (TrO), post-projection of l, pre-projection of l+1
             o1 = self.o1_h.to(x1.device, non_blocking=True)
             x1 = W.post(x1, o1)
@@ -273,8 +277,8 @@ class GraphedPipeline(AsymmetricPipeline):
     two replays. Every graph reads and writes fixed buffers, so each replay
     recomputes the iteration from the batches' stored hidden states."""
 
-    def __init__(self, layers, gpu, cpu, *, cpu_threads: int = 0):
-        super().__init__(layers, gpu, cpu, cpu_threads=cpu_threads)
+    def __init__(self, layers, gpu, cpu, *, cpu_threads: int = 0, cpu_isa: str = "auto"):
+        super().__init__(layers, gpu, cpu, cpu_threads=cpu_threads, cpu_isa=cpu_isa)
         torch = self.torch
         g, c, Ls = gpu, cpu, layers
         self._keep = []

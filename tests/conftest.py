@@ -8,3 +8,11 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+
+
+def pytest_terminal_summary(terminalreporter):
+    from parity_report import LINES
+    if LINES:
+        terminalreporter.write_sep("-", "errors against the fp64 oracle")
+        for line in LINES:
+            terminalreporter.write_line(line)

@@ -58,6 +58,32 @@ def test_workspace_bytes_grow_with_batch_and_group():
     assert a >= 2 * neo.MAX_SLICES * 4 * 129 * 4
 
 
+def _align256(x):
+    return (x + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("batch,hq,hkv", [(0, 8, 8), (1, 32, 32), (64, 32, 8), (512, 64, 8),
+                                          (1024, 32, 8), (3000, 128, 8)])
+def test_workspace_bytes_match_the_documented_formula(batch, hq, hkv):
+    # The header states the size: a fixed part sized for NEO_MAX_SLICES, one
+    # int32 per request, and two partial slots per slice of group rows of
+    # head_dim floats plus group log-sum-exps; no dependence on lengths or pool.
+    S, D, G = neo.MAX_SLICES, 128, hq // hkv
+    want = (_align256(16) + _align256(32 * (S + 1)) + _align256(4 * S) +
+            _align256(4 * (batch + 1)) + _align256(8 * S * G) + _align256(8 * S * G * D))
+    assert neo.workspace_bytes(batch, hq, hkv) == want
+
+
+def test_header_documents_the_workspace_contract():
+    text = open(HEADER).read()
+    # The fused default is one kernel; the workspace is zeroed once and keeps
+    # counters between calls.
+    assert "Enqueues one kernel" in text
+    assert "Enqueues two kernels" not in text
+    assert "zero-filled once before its first use" in text
+    assert "align256(8 * NEO_MAX_SLICES * group * head_dim)" in text
+
+
 @pytest.mark.parametrize("args,code", [
     ((64, 32, 7, 128), INVALID),
     ((64, 0, 8, 128), INVALID),
@@ -112,6 +138,7 @@ def call(lib, **kw):
     (dict(slices=-1), INVALID, "max_slices"),
     (dict(slices=100000), INVALID, "max_slices"),
     (dict(batch=1 << 20, mbps=1 << 12), INVALID, "2^31"),
+    (dict(batch=1 << 18, mbps=(1 << 10) - 3), INVALID, "+ 3)"),
 ])
 def test_decode_rejects_bad_arguments_before_any_hip_call(lib, kw, code, needle):
     assert call(lib, **kw) == code

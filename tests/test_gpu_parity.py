@@ -5,14 +5,17 @@ Bar (decode attention with bf16 q/K/V and fp32 accumulation): max abs error
 max_d |y - r| / max_d |r|); block-table indexing bit-exact (the gather kernel,
 and bit-identical outputs under physical-block relabeling).
 """
+import ctypes
 import math
 import sys
+import time
 
 import numpy as np
 import pytest
 
 import oracle
 import paper_2411_01142_amd as neo
+from parity_report import record
 from paper_2411_01142_amd import workloads as W
 
 torch = pytest.importorskip("torch")
@@ -130,44 +133,28 @@ def test_softmax_range_stress(variant):
 
 # --------------------------------------------------------------------- parity, configs
 
-def sample_rows(case, n, seed):
-    rng = np.random.default_rng(seed)
-    Hq = case.num_q_heads
-    longest = np.argsort(-case.seq_lens.astype(np.int64))[:8]
-    rows = {int(b) * Hq + h for b in longest for h in (0, Hq - 1)}
-    rows |= set(int(x) for x in rng.choice(case.batch * Hq, size=n, replace=False))
-    return np.array(sorted(rows))
-
-
-def oracle_rows(case, rows):
-    ref = np.zeros((case.batch * case.num_q_heads, case.head_dim), dtype=np.float32)
-    for r in rows:
-        ref[r] = oracle.decode_attention(case, rows=(int(r), int(r) + 1)).reshape(
-            -1, case.head_dim)[r]
-    return ref
-
-
-@pytest.mark.parametrize("cfg,seed,batch_limit", [
-    (1, 1, None), (1, 101, None), (2, 2, None), (2, 102, None),
-    (3, 3, None), (3, 103, None), (4, 4, None), (4, 104, 96),
-    (5, 5, None), (5, 105, None),
+@pytest.mark.parametrize("cfg,seed", [
+    (1, 1), (1, 101), (2, 2), (2, 102), (3, 3), (3, 103), (4, 4), (4, 104), (5, 5), (5, 105),
 ])
-def test_config_parity(cfg, seed, batch_limit):
-    say(f"[config] cfg={cfg} seed={seed} batch_limit={batch_limit}: generating")
-    case = W.make_config(cfg, seed, batch_limit=batch_limit)
-    say(f"[config] {case.name} B={case.batch} NB={case.num_blocks} sumL={case.total_tokens()}")
-    y = run(case).reshape(-1, case.head_dim)
-    if cfg in (1, 2):
-        ref = oracle.decode_attention(case).reshape(-1, case.head_dim)
-        assert_parity(y, ref, case.name)
-    else:
-        rows = sample_rows(case, 48, seed)
-        ref = oracle_rows(case, rows)
-        assert_parity(y, ref, case.name + f" ({len(rows)} sampled rows)", rows=rows)
-        # Properties at any size: every row finite and inside the convex hull
-        # bound of V (|out| <= max |V| over valid rows <= 4.5 for these inputs).
-        assert np.all(np.isfinite(y))
-        assert np.abs(y).max() <= 4.5
+def test_config_parity(cfg, seed):
+    # Every row of every workload at full size, in the launch the benchmark
+    # times (default schedule and slice count): the large batches are the only
+    # runs of the default plan's XCD-weighted slices and of cut pairs merged
+    # across workgroups with many contributors. The oracle runs on all host
+    # cores (a few hundred ms per batch on a 16-core host).
+    say(f"[config] cfg={cfg} seed={seed}: generating")
+    t0 = time.perf_counter()
+    case = W.make_config(cfg, seed)
+    say(f"[config] {case.name} B={case.batch} NB={case.num_blocks} sumL={case.total_tokens()} "
+        f"(generated in {time.perf_counter() - t0:.1f} s)")
+    y = run(case)
+    t0 = time.perf_counter()
+    ref = oracle.decode_attention(case)
+    say(f"[config] oracle over {case.batch * case.num_q_heads} rows in "
+        f"{time.perf_counter() - t0:.1f} s")
+    ae, re = assert_parity(y, ref, f"{case.name} (all {case.batch * case.num_q_heads} rows)")
+    record(f"{case.name}: all {case.batch * case.num_q_heads} rows, max_abs={ae:.2e} "
+           f"max_rel_rownorm={re:.2e}")
 
 
 # --------------------------------------------------------------------- edge cases
@@ -414,6 +401,48 @@ def test_runs_on_a_side_stream():
         out = neo.decode_attention(q, k, v, bt, sl, scale=case.scale)
     s.synchronize()
     assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_workspace_init_through_the_c_abi():
+    # A workspace full of stale bytes (arrival counters included) is cleared by
+    # neo_decode_workspace_init on the call's stream; every later call then
+    # leaves the counters at zero for the next one.
+    case = W.build_case([100, 2000, 37, 900, 3000, 16], 16, 4, 128, 16, seed=16)
+    ref = oracle.decode_attention(case)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    lib = neo.load_library()
+    n = neo.workspace_bytes(case.batch, case.num_q_heads, case.num_kv_heads)
+    ws = torch.full((n,), 0x5A, dtype=torch.uint8, device="cuda")
+    out = torch.empty((case.batch, case.num_q_heads, 128), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    sh = ctypes.c_void_p(s.cuda_stream)
+    assert lib.neo_decode_workspace_init(ws.data_ptr(), n, sh) == 0
+    for i in range(3):
+        rc = lib.neo_decode_attention(q.data_ptr(), k.data_ptr(), v.data_ptr(), bt.data_ptr(),
+                                      sl.data_ptr(), case.num_q_heads, case.num_kv_heads, 128,
+                                      16, float(case.scale), out.data_ptr(), case.batch,
+                                      case.max_blocks_per_seq, case.num_blocks, ws.data_ptr(),
+                                      n, sh)
+        assert rc == 0, lib.neo_last_error()
+        s.synchronize()
+        assert_parity(out.cpu().numpy(), ref, f"workspace init, call {i}")
+
+
+def test_cached_workspace_is_cleared_on_the_call_stream():
+    # The binding's cached workspace for a new stream is allocated in that
+    # stream's pool and cleared on it, so the first call there sees zeroed
+    # counters even when the stream starts with no dependency on another.
+    case = W.build_case([700, 1500, 9, 2500], 32, 8, 128, 16, seed=17)
+    ref = oracle.decode_attention(case)
+    q, k, v, bt, sl = case.to_torch("cuda")
+    torch.cuda.synchronize()
+    for _ in range(2):
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            out = neo.decode_attention(q, k, v, bt, sl, scale=case.scale)
+        s.synchronize()
+        assert_parity(out.cpu().numpy(), ref, "cached workspace on a new stream")
 
 
 def test_binding_errors_are_raised():

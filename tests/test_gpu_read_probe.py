@@ -1,4 +1,4 @@
-"""GPU test of the streaming-read probe (the measurement aid behind
+"""GPU test of the two read probes (the measurement aids behind
 `bench.py --op read_ceiling`): it must read every 16-byte word exactly once,
 which the xor of its per-wave sink words shows."""
 import sys
@@ -45,3 +45,32 @@ def test_read_probe_binding_checks():
         neo.read_probe(src, torch.zeros(8, dtype=torch.int32, device="cuda"))
     with pytest.raises(ValueError):
         neo.read_probe(src.cpu(), torch.zeros(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32))
+
+
+# One step (most waves empty), a count that leaves waves with unequal ranges,
+# and several rounds of every depth's ring.
+@pytest.mark.parametrize("nbytes", [8192, 8192 * 1237, 1 << 27])
+@pytest.mark.parametrize("wpc,depth", [(4, 1), (8, 2), (12, 3), (8, 4), (16, 1)])
+def test_tile_probe_reads_every_word_once(nbytes, wpc, depth):
+    print(f"[probe-tiles] bytes={nbytes} waves/CU={wpc} depth={depth}", flush=True)
+    sys.stdout.flush()
+    rng = np.random.default_rng(nbytes + wpc + depth)
+    host = rng.integers(0, 2 ** 32, nbytes // 4, dtype=np.uint32)
+    src = torch.from_numpy(host.view(np.int32)).cuda()
+    sink = torch.zeros(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
+    neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth)
+    torch.cuda.synchronize()
+    words = sink.cpu().numpy().view(np.uint32)
+    assert np.bitwise_xor.reduce(words) == np.bitwise_xor.reduce(host)
+
+
+def test_tile_probe_rejects_bad_arguments():
+    src = torch.zeros(4096, dtype=torch.int32, device="cuda")   # 16 KiB
+    sink = torch.zeros(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
+    for kw in (dict(waves_per_cu=6), dict(waves_per_cu=20), dict(depth=0), dict(depth=5)):
+        with pytest.raises(neo.NeoError):
+            neo.read_probe_tiles(src, sink, **kw)
+    with pytest.raises(neo.NeoError):
+        neo.read_probe_tiles(src[:100], sink)                  # not a multiple of 8192 bytes
+    with pytest.raises(neo.NeoError):
+        neo.read_probe_tiles(src, sink[:16])                   # sink too small

@@ -178,6 +178,29 @@ def test_softmax_weights_sum_to_one(seed):
             assert abs(w.sum() - 1.0) <= 1e-12
 
 
+@pytest.mark.parametrize("lens,hq,hkv,seed", [
+    ([1, 16, 17, 300], 8, 2, 0),
+    ([5, 64, 129], 16, 4, 1),
+    ([40, 2], 4, 4, 2),
+])
+def test_softmax_weights_match_torch_softmax(lens, hq, hkv, seed):
+    # The weights themselves, position by position, against torch's fp64
+    # softmax of scale * q K^T over the dense K the generator's own layout code
+    # unpacks (so a permuted, shifted or mis-indexed weight vector fails).
+    case = W.build_case(lens, hq, hkv, 128, 16, seed=seed, k_outlier_frac=0.05)
+    q = W.bf16_to_f32(case.q).astype(np.float64)
+    G = case.group
+    for b, (K, _) in enumerate(dense_kv(case)):
+        for h in range(hq):
+            s = torch.from_numpy(K[h // G] @ q[b, h]) * case.scale
+            ref = torch.softmax(s, dim=0).numpy()
+            w = oracle.softmax_weights(case, b, h)
+            assert w.shape == ref.shape
+            assert np.max(np.abs(w - ref)) <= 1e-13, (b, h)
+            # The largest weight sits at the largest score.
+            assert int(np.argmax(w)) == int(torch.argmax(s))
+
+
 def _relabel(case, rng):
     """Move every physical block to a new id; rewrite the table to match."""
     nb = case.num_blocks
