@@ -181,6 +181,33 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        void* stream);
 
 /*
+ * For callers that cannot allocate device memory or a workspace (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * neo_decode_attention without the workspace arguments. The same operation,
+ * layouts, checks and clamping rules, and the same single fused kernel
+ * (MFMA family, default slice policy capped at 1024 slices); for a given
+ * input the result equals neo_decode_attention's up to fp32 summation order
+ * (bit for bit on a part with at most 256 compute units).
+ * Instead of a workspace it uses a file-scope device array of the library
+ * (16.1 MiB per GPU, held until the process ends): the arrival counters and
+ * partial outputs of requests split across workgroups, for up to 1024 slices
+ * at any supported query group (a larger group would be refused with
+ * NEO_ERR_WORKSPACE). Its address on each device is looked up on the first
+ * call made with that device current, which also clears its counters on
+ * `stream`; every call leaves them at zero again. It calls no hipMalloc or
+ * hipFree and no allocating library routine. Every call on one GPU shares
+ * that GPU's array: calls that may overlap on one GPU (different streams with
+ * no ordering between them, or different host threads) race and give wrong
+ * results; order them, or use neo_decode_attention with distinct workspaces.
+ */
+neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                        const int32_t* block_table, const int32_t* seq_lens,
+                                        int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t block_size, float scale,
+                                        float* out, int32_t batch, int32_t max_blocks_per_seq,
+                                        int32_t num_blocks, void* stream);
+
+/*
  * Bit-exact dense copy of one paged cache through the block table (the paged
  * layout of Sec. 2.1 / Sec. 4). is_v = 0 reads the K layout, 1 the V layout.
  * token_offsets: device int32 [batch+1], exclusive prefix sum of seq_lens

@@ -89,6 +89,8 @@ def load_library():
         lib.neo_decode_attention_events.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P,
                                                     S, I, I, I, P, P, P]
         lib.neo_decode_attention_events.restype = ctypes.c_int
+        lib.neo_decode_attention_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P]
+        lib.neo_decode_attention_noalloc.restype = ctypes.c_int
         lib.neo_decode_workspace_init.argtypes = [P, S, P]
         lib.neo_decode_workspace_init.restype = ctypes.c_int
         lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, P, P]

@@ -7,6 +7,7 @@
 #include <stdio.h>
 
 #include <atomic>
+#include <mutex>
 #include <string>
 
 #include "neo_error.h"
@@ -127,6 +128,109 @@ neo_status check_heads(int32_t hq, int32_t hkv, int32_t head_dim) {
   return NEO_OK;
 }
 
+// Host-side checks of a decode call, shared by every decode entry point (no
+// HIP call). *noop is set for an empty batch, which needs no pointer.
+neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* block_table, const int32_t* seq_lens,
+                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                        int32_t block_size, float scale, const float* out, int32_t batch,
+                        int32_t max_blocks_per_seq, int32_t num_blocks, int32_t variant,
+                        int32_t schedule, int32_t max_slices, bool* noop) {
+  *noop = false;
+  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
+  const neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
+  if (st != NEO_OK) return st;
+  if (block_size != neo::kBlock)
+    return set_error(NEO_ERR_UNSUPPORTED, "block_size %d unsupported (only %d)", block_size,
+                     neo::kBlock);
+  if (!isfinite(scale)) return set_error(NEO_ERR_INVALID_ARG, "scale is not finite");
+  if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
+    return set_error(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
+  if (schedule != NEO_SCHEDULE_AUTO && schedule != NEO_SCHEDULE_FUSED &&
+      schedule != NEO_SCHEDULE_STAGED && schedule != NEO_SCHEDULE_TWO_KERNEL)
+    return set_error(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
+  if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
+    return set_error(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
+                     NEO_MAX_SLICES);
+  if (batch == 0) {
+    *noop = true;
+    return ok();
+  }
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
+                     max_blocks_per_seq, num_blocks);
+  if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCostLong) * num_kv_heads >= ((int64_t)1 << 31))
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "batch * (max_blocks_per_seq + %d) * num_kv_heads must stay below 2^31",
+                     neo::kPairCostLong);
+  if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
+    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
+    return set_error(NEO_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
+    return set_error(NEO_ERR_INVALID_ARG, "block_table and seq_lens must be 4-byte aligned");
+  return NEO_OK;
+}
+
+// ----------------------------------------------------------------- static scratch
+//
+// The allocation-free entry point keeps the fused kernel's cross-workgroup
+// merge state in a file-scope device array instead of a caller workspace:
+// the arrival counters of cut pairs (one int32 per slice) and two partial
+// slots per slice (group rows of head_dim floats plus group log-sum-exps).
+// It is sized for kScratchSlices slices at the largest supported group; the
+// plan of that entry point uses at most kScratchSlices slices (one per wave
+// of one 4-wave workgroup per CU on a 256-CU part). Every GPU the library
+// runs on holds one copy until the process ends (16.1 MiB).
+constexpr int32_t kScratchSlices = 1024;
+constexpr int32_t kScratchMaxGroup = 16;
+constexpr size_t kScratchCountersOff = 0;
+constexpr size_t kScratchLseOff =
+    kScratchCountersOff + ((sizeof(int32_t) * kScratchSlices + 255) & ~size_t(255));
+constexpr size_t kScratchOOff =
+    kScratchLseOff + ((sizeof(float) * 2 * kScratchSlices * kScratchMaxGroup + 255) & ~size_t(255));
+constexpr size_t kScratchBytes =
+    kScratchOOff + sizeof(float) * 2 * kScratchSlices * kScratchMaxGroup * neo::kHeadDim;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on each device ordinal (the host-side name is
+// only a stand-in, never a device address), looked up once per device with
+// that device current; set-up also clears the arrival counters, which every
+// call then leaves at zero.
+std::mutex g_scratch_mutex;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+neo_status scratch_address(hipStream_t stream, char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(NEO_ERR_HIP, "device ordinal %d outside [0, %d)", dev, kMaxDevices);
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void* ptr = nullptr;
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !ptr)
+        return set_error(NEO_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      e = neo::launch_fill_zero(static_cast<char*>(ptr) + kScratchCountersOff,
+                                sizeof(int32_t) * kScratchSlices, stream);
+      if (e != hipSuccess)
+        return set_error(NEO_ERR_HIP, "scratch counter fill: %s", hipGetErrorString(e));
+      g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+      p = ptr;
+    }
+  }
+  *out = static_cast<char*>(p);
+  return NEO_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -155,38 +259,12 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        int32_t schedule, int32_t max_slices,
                                        void* decode_start_event, void* decode_end_event,
                                        void* stream) {
-  if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
-  neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
-  if (st != NEO_OK) return st;
-  if (block_size != neo::kBlock)
-    return set_error(NEO_ERR_UNSUPPORTED, "block_size %d unsupported (only %d)", block_size,
-                     neo::kBlock);
-  if (!isfinite(scale)) return set_error(NEO_ERR_INVALID_ARG, "scale is not finite");
-  if (variant != NEO_VARIANT_AUTO && variant != NEO_VARIANT_VALU && variant != NEO_VARIANT_MFMA)
-    return set_error(NEO_ERR_UNSUPPORTED, "unknown variant %d", variant);
-  if (schedule != NEO_SCHEDULE_AUTO && schedule != NEO_SCHEDULE_FUSED &&
-      schedule != NEO_SCHEDULE_STAGED && schedule != NEO_SCHEDULE_TWO_KERNEL)
-    return set_error(NEO_ERR_UNSUPPORTED, "unknown schedule %d", schedule);
-  if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
-    return set_error(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
-                     NEO_MAX_SLICES);
-  if (batch == 0) return ok();
-  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
-    return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
-  if (max_blocks_per_seq <= 0 || num_blocks <= 0)
-    return set_error(NEO_ERR_INVALID_ARG,
-                     "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
-                     max_blocks_per_seq, num_blocks);
-  if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCostLong) * num_kv_heads >= ((int64_t)1 << 31))
-    return set_error(NEO_ERR_INVALID_ARG,
-                     "batch * (max_blocks_per_seq + %d) * num_kv_heads must stay below 2^31",
-                     neo::kPairCostLong);
-  if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
-    return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
-  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
-    return set_error(NEO_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
-  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
-    return set_error(NEO_ERR_INVALID_ARG, "block_table and seq_lens must be 4-byte aligned");
+  bool noop = false;
+  neo_status st = check_decode(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
+                               num_kv_heads, head_dim, block_size, scale, out, batch,
+                               max_blocks_per_seq, num_blocks, variant, schedule, max_slices,
+                               &noop);
+  if (st != NEO_OK || noop) return st;
   const int32_t group = num_q_heads / num_kv_heads;
   const neo::WorkspaceLayout wl = neo::workspace_layout(batch, group);
   if (!workspace || workspace_bytes < wl.total)
@@ -289,6 +367,61 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
                                      max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
                                      NEO_VARIANT_AUTO, NEO_SCHEDULE_AUTO, 0, nullptr, nullptr,
                                      stream);
+}
+
+neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                        const int32_t* block_table, const int32_t* seq_lens,
+                                        int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t block_size, float scale,
+                                        float* out, int32_t batch, int32_t max_blocks_per_seq,
+                                        int32_t num_blocks, void* stream) {
+  bool noop = false;
+  neo_status st = check_decode(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
+                               num_kv_heads, head_dim, block_size, scale, out, batch,
+                               max_blocks_per_seq, num_blocks, NEO_VARIANT_AUTO,
+                               NEO_SCHEDULE_AUTO, 0, &noop);
+  if (st != NEO_OK || noop) return st;
+  const int32_t group = num_q_heads / num_kv_heads;
+  if (group > kScratchMaxGroup)
+    return set_error(NEO_ERR_WORKSPACE, "query group %d exceeds the static scratch (at most %d)",
+                     group, kScratchMaxGroup);
+  int32_t cus = 0, xcds = 0;
+  st = device_shape(&cus, &xcds);
+  if (st != NEO_OK) return st;
+  const int32_t quantum = cus * neo::kWavesPerGroup;
+  // The default slice policy, capped at what the scratch holds.
+  const int32_t slices = std::min<int32_t>(quantum, kScratchSlices);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = nullptr;
+  st = scratch_address(s, &base);
+  if (st != NEO_OK) return st;
+
+  neo::DecodeParams p;
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.table = block_table;
+  p.lens = seq_lens;
+  p.out = out;
+  p.hdr = nullptr;     // plan records: staged and two-kernel launches only
+  p.starts = nullptr;
+  p.part_lse = reinterpret_cast<float*>(base + kScratchLseOff);
+  p.part_o = reinterpret_cast<float*>(base + kScratchOOff);
+  p.counters = reinterpret_cast<int32_t*>(base + kScratchCountersOff);
+  p.batch = batch;
+  p.hq = num_q_heads;
+  p.hkv = num_kv_heads;
+  p.mbps = max_blocks_per_seq;
+  p.num_blocks = num_blocks;
+  p.max_slices = slices;
+  p.min_tiles = 0;
+  p.slice_quantum = quantum;
+  p.xcd8 = xcds == 8;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
+  const hipError_t e = neo::launch_decode_mfma(p, group, neo::kFused, grid, s);
+  if (e != hipSuccess) return set_error(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
 }
 
 neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {

@@ -244,3 +244,20 @@ def test_python_binding_refuses_cpu_tensors():
     sl = torch.ones(2, dtype=torch.int32)
     with pytest.raises(ValueError, match="GPU"):
         neo.decode_attention(q, k, v, bt, sl)
+
+
+def test_noalloc_entry_point_checks_arguments_before_any_hip_call(lib):
+    def na(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, table=FAKE, lens=FAKE, hq=32, hkv=8, d=128, bs=16,
+                 scale=0.1, out=FAKE, batch=4, mbps=8, nb=100)
+        a.update(kw)
+        return lib.neo_decode_attention_noalloc(a["q"], a["k"], a["v"], a["table"], a["lens"],
+                                                a["hq"], a["hkv"], a["d"], a["bs"], a["scale"],
+                                                a["out"], a["batch"], a["mbps"], a["nb"], None)
+    assert na(hkv=7) == INVALID
+    assert na(d=64) == UNSUPPORTED
+    assert na(bs=8) == UNSUPPORTED
+    assert na(scale=float("nan")) == INVALID
+    assert na(out=None) == INVALID
+    assert na(q=FAKE + 4) == INVALID
+    assert na(batch=0, q=None, k=None, v=None, table=None, lens=None, out=None) == OK
