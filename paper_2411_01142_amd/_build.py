@@ -15,9 +15,10 @@ LIB = os.path.join(PKG, "libneoattn.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["api.hip", "plan_combine.hip", "decode_mfma.hip", "decode_valu.hip", "kv_ops.hip"]
-# Host-only C++ (the CPU attention), built with the host compiler; its
-# ISA-specific functions carry target attributes and are picked at run time.
-HOST_SOURCES = ["cpu_attention.cpp", "scheduler.cpp"]
+# Host-only C++ (the CPU attention, the scheduler, the error text), built with
+# the host compiler; the CPU attention's ISA-specific functions carry target
+# attributes and are picked at run time.
+HOST_SOURCES = ["cpu_attention.cpp", "scheduler.cpp", "neo_error.cpp"]
 HOST_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-pthread", "-fno-math-errno",
               "-I" + INCLUDE, "-I" + CSRC]
 

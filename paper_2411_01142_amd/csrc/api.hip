@@ -1,41 +1,15 @@
 // C ABI of libneoattn: argument checks (all on the host, before any HIP
 // call), workspace sizing and the launch sequence plan -> decode -> combine.
 #include <math.h>
-#include <stdarg.h>
 
 #include <algorithm>
-#include <stdio.h>
-
 #include <atomic>
 #include <mutex>
-#include <string>
 
 #include "neo_error.h"
 #include "kv_ops.h"
 #include "neo_internal.h"
 
-namespace {
-thread_local std::string g_last_error;
-}  // namespace
-
-namespace neo {
-
-neo_status set_error(neo_status st, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  return st;
-}
-
-neo_status clear_error() {
-  g_last_error.clear();
-  return NEO_OK;
-}
-
-}  // namespace neo
 
 namespace {
 
@@ -234,8 +208,6 @@ neo_status scratch_address(hipStream_t stream, char** out) {
 }  // namespace
 
 extern "C" {
-
-const char* neo_last_error(void) { return g_last_error.c_str(); }
 
 const char* neo_version(void) { return "0.1.0"; }
 
