@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 }
 
 // Staged launch: aggregation of the partial outputs of pairs cut by slice
-// boundaries (Sec. 4: "aggregate the partial outputs of each request"). Wave
+// boundaries (Sec. 4: the per-request partial results are combined). Wave
 // w looks at boundary s = w + 1: when it falls strictly inside the tiles of a
 // pair whose first tile lies in slice s - 1, that boundary is the first to cut
 // the pair and the wave merges it. Every contributing slice stored its part

@@ -269,7 +269,7 @@ def merge_caches(gpu: GpuBatch, cpu: CpuBatch, layers):
 
 class GraphedPipeline(AsymmetricPipeline):
     """The same schedule with each stage's GPU work captured once as a HIP
-    graph and replayed (launch overhead off the critical path, Sec. 4 "Reducing
+    graph and replayed (launch overhead off the critical path, Sec. 4, "Reducing
     Kernel Launching Overhead"): per layer, graph A (batch-0: post-projection
     of l-1, pre-projection of l, append, attention) and graph B (batch-1: TrO,
     post-projection of l, pre-projection of l+1, TrQKV), plus a prologue and an

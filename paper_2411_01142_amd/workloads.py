@@ -7,7 +7,7 @@ module that both the HIP path's tests and the fp64 oracle's tests take inputs
 from.
 
 Storage contract (the paged KV cache of Sec. 2.1 and Sec. 4 of the paper,
-which stores KV "similar to vLLM"):
+whose layout the paper likens to vLLM's):
 
 * ``q``           bf16 ``[batch][num_q_heads][head_dim]``
 * ``k_cache``     bf16 ``[num_blocks][num_kv_heads][head_dim/8][block_size][8]``

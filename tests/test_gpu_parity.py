@@ -186,6 +186,32 @@ def test_batch_of_one_long_request():
         assert_parity(run(case, variant=variant), ref, f"B=1 L=9000 {variant}")
 
 
+def test_maximum_sizes_many_requests_and_one_very_long_request():
+    # Sizes beyond every workload: 16384 requests of 0-64 tokens (the in-kernel
+    # plan reads the lengths in 16 rounds of 1024 requests; most pairs are one
+    # block), then one request of 131072 tokens at group 8 (8192 blocks per
+    # pair, every slice of the default plan inside one of its 8 pairs, cut
+    # pairs merged with ~128 contributors each). Every row against the oracle.
+    rng = np.random.default_rng(51)
+    lens = rng.integers(0, 65, 16384)
+    lens[rng.random(16384) < 0.05] = 0
+    case = W.build_case(lens.tolist(), 8, 2, 128, 16, seed=51)
+    say(f"[max] B={case.batch} sumL={case.total_tokens()}")
+    ref = oracle.decode_attention(case)
+    for variant in ("mfma", "valu"):
+        a = run(case, variant=variant)
+        ae, re = assert_parity(a, ref, f"16384 short requests {variant}")
+        record(f"16384 requests of 0-64 tokens ({variant}): max_abs={ae:.2e} max_rel_rownorm={re:.2e}")
+    case = W.build_case([131072], 64, 8, 128, 16, seed=52)
+    say(f"[max] B=1 L=131072 G=8")
+    ref = oracle.decode_attention(case)
+    for variant in ("mfma", "valu"):
+        a = run(case, variant=variant)
+        ae, re = assert_parity(a, ref, f"one request of 131072 tokens {variant}")
+        record(f"one request of 131072 tokens, G=8 ({variant}): max_abs={ae:.2e} "
+               f"max_rel_rownorm={re:.2e}")
+
+
 def test_lengths_beyond_the_table_are_clamped():
     case = W.build_case([40, 64], 4, 2, 128, 16, seed=9)
     clamped = W.Case(**{**case.__dict__, "seq_lens": np.array([40, 64], np.int32)})
