@@ -1,5 +1,8 @@
 // C ABI of libneoattn: argument checks (all on the host, before any HIP
-// call), workspace sizing and the launch sequence plan -> decode -> combine.
+// call), workspace sizing, and the launches: by default one fused decode
+// kernel (plan, tiles and merges), or plan -> decode -> combine (staged) and
+// decode -> combine (two-kernel); the allocation-free entry point and its
+// static scratch; the cache operations and the read probes.
 #include <math.h>
 
 #include <algorithm>

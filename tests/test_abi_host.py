@@ -261,3 +261,13 @@ def test_noalloc_entry_point_checks_arguments_before_any_hip_call(lib):
     assert na(out=None) == INVALID
     assert na(q=FAKE + 4) == INVALID
     assert na(batch=0, q=None, k=None, v=None, table=None, lens=None, out=None) == OK
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    # No fallback: with the shared library absent every entry point raises.
+    monkeypatch.setattr(neo, "_LIB_PATH", str(tmp_path / "missing_libneoattn.so"))
+    monkeypatch.setattr(neo, "_lib", None)
+    with pytest.raises(ImportError):
+        neo.load_library()
+    with pytest.raises(ImportError):
+        neo.workspace_bytes(4, 32, 8)
