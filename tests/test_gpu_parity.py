@@ -391,6 +391,44 @@ def test_random_shapes(i):
     assert np.array_equal(a, b), f"random {i}: fused != two_kernel"
 
 
+def large_random_case(i):
+    rng = np.random.default_rng(5000 + i)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    group = [1, 2, 4, 8, 16][i % 5]
+    batch = int(rng.integers(64, 2049))
+    mix = i % 3  # uniform long, lognormal, few very long among short
+    if mix == 0:
+        lens = rng.integers(200, 6000, batch)
+    elif mix == 1:
+        lens = np.clip(np.round(1200 * np.exp(0.8 * rng.standard_normal(batch))), 1, 20000)
+    else:
+        lens = np.where(rng.random(batch) < 0.02, rng.integers(8000, 30000, batch),
+                        rng.integers(0, 300, batch))
+    lens = lens.astype(np.int64)
+    # At most ~2M (token, kv head) pairs: ~1 GB of KV, a fraction of a second of oracle.
+    while int(lens.sum()) * hkv > 2_000_000 and batch > 8:
+        batch //= 2
+        lens = lens[:batch]
+    return W.build_case(lens.tolist(), hkv * group, hkv, 128, 16, seed=6000 + i, poison=True)
+
+
+@pytest.mark.parametrize("i", range(15))
+def test_large_random_batches(i):
+    # Seeded batches at the workloads' scale with the groups they lack (1, 2, 16 beside 4 and
+    # 8), 1-8 kv heads, up to 2048 requests, in the default launch: every row against the
+    # oracle, and the fused schedule equal to the two-kernel one bit for bit.
+    case = large_random_case(i)
+    say(f"[large] case {i}: B={case.batch} Hq={case.num_q_heads} Hkv={case.num_kv_heads} "
+        f"sumL={case.total_tokens()}")
+    ref = oracle.decode_attention(case)
+    a = run(case)
+    ae, re = assert_parity(a, ref, f"large random {i}")
+    record(f"large random {i} (B={case.batch}, G={case.group}, Hkv={case.num_kv_heads}): "
+           f"max_abs={ae:.2e} max_rel_rownorm={re:.2e}")
+    b = run(case, schedule="two_kernel")
+    assert np.array_equal(a, b), f"large random {i}: fused != two_kernel"
+
+
 def test_poisoned_slots_do_not_leak():
     lens = [1, 15, 17, 64, 99, 250]
     a = W.build_case(lens, 16, 4, 128, 16, seed=12, poison=True)
