@@ -6,7 +6,7 @@ layer. The default workload is the largest one-GPU configuration, the
 Llama-3.1-70B layer shape (64 q heads, 8 kv heads, head_dim 128, block 16),
 batch 512, lengths uniform in [256, 4096] (the paper's 70B setting, Sec. 5.1,
 with code-generation-like lengths), shuffled physical blocks, bf16 q/K/V
-~ N(0,1) (synthetic, seeded): 4.6 GB of KV per call. `--config 1..5` picks
+~ N(0,1) (synthetic, seeded): 4.6 GB of KV per call. `--config 1..6` picks
 the other workloads.
 
 Inputs are resident in HBM before timing. The KV cache is replicated (at least
@@ -45,7 +45,8 @@ MALL_BYTES = 256 * 2 ** 20     # Infinity Cache
 METRIC = "decode-attention achieved HBM GB/s (% of peak) + tokens/sec per layer, 1 GPU"
 KERNEL_SOURCES = ("decode_mfma.hip", "decode_valu.hip", "decode_common.h", "neo_internal.h")
 SEQ_DESC = {1: "U[64,512]", 2: "U[512,2048]", 3: "lognormal(median 1500, sigma 0.6) clip [128,8192]",
-            4: "U[256,4096]", 5: "8 x 32768 + 1016 x U[16,256]"}
+            4: "U[256,4096]", 5: "8 x 32768 + 1016 x U[16,256]",
+            6: "U[256,4096] (one GPU's share of the 70B layer at 8-way tensor parallelism)"}
 
 
 def log(msg):
@@ -640,7 +641,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-flush-pass", action="store_true",
                     help="skip the per-call pass with a 1 GiB read before each call")
     ap.add_argument("--seed", type=int, default=None)

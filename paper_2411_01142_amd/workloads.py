@@ -278,9 +278,10 @@ def build_case(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
 
 
 # --------------------------------------------------------------------------------------
-# The five layer-shaped workloads. Shapes: LLaMa-2-7B (32 q / 32 kv heads),
-# LLaMa-3-8B (32 / 8), LLaMa-3.1-70B (64 / 8); head_dim 128, block_size 16,
-# bf16 q/K/V ~ N(0,1), scale 1/sqrt(128), shuffled physical blocks.
+# The five layer-shaped workloads, and one GPU's share of the 70B layer under
+# 8-way tensor parallelism. Shapes: LLaMa-2-7B (32 q / 32 kv heads), LLaMa-3-8B
+# (32 / 8), LLaMa-3.1-70B (64 / 8; its TP-8 share 8 / 1); head_dim 128,
+# block_size 16, bf16 q/K/V ~ N(0,1), scale 1/sqrt(128), shuffled physical blocks.
 # --------------------------------------------------------------------------------------
 
 def _lens_cfg1(rng):
@@ -321,6 +322,10 @@ CONFIGS = {
             k_outlier_frac=0.0),
     5: dict(name="llama3-8b_b1024_skew8x32k", num_q_heads=32, num_kv_heads=8, lens=_lens_cfg5,
             k_outlier_frac=0.0),
+    # One GPU's share of the 70B layer under 8-way tensor parallelism (each GPU holds one kv
+    # head and its 8 query heads): configuration 4's lengths and draw order, 1/8 of its KV.
+    6: dict(name="llama3.1-70b-tp8share_b512_u256-4096", num_q_heads=8, num_kv_heads=1,
+            lens=_lens_cfg4, k_outlier_frac=0.0),
 }
 
 
@@ -331,7 +336,7 @@ def config_seq_lens(cfg: int, seed: int) -> np.ndarray:
 
 def make_config(cfg: int, seed: Optional[int] = None, *, poison: bool = True,
                 batch_limit: Optional[int] = None) -> Case:
-    """Config ``cfg`` (1..5) with seed ``seed`` (default: ``cfg``).
+    """Config ``cfg`` (1..6) with seed ``seed`` (default: ``cfg``).
 
     ``batch_limit`` keeps only the first requests (the draw order is unchanged
     for the lengths; later draws then cover the smaller batch).

@@ -135,6 +135,7 @@ def test_softmax_range_stress(variant):
 
 @pytest.mark.parametrize("cfg,seed", [
     (1, 1), (1, 101), (2, 2), (2, 102), (3, 3), (3, 103), (4, 4), (4, 104), (5, 5), (5, 105),
+    (6, 6), (6, 106),
 ])
 def test_config_parity(cfg, seed):
     # Every row of every workload at full size, in the launch the benchmark
