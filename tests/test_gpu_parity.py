@@ -392,6 +392,50 @@ def test_random_shapes(i):
     assert np.array_equal(a, b), f"random {i}: fused != two_kernel"
 
 
+def mixed_random_case(i):
+    """Shapes beyond the power-of-two kv head counts (3, 5, 16 kv heads), lengths
+    around block multiples, runs of 0-1 token requests, equal lengths, a few long
+    requests among short ones; random kernel family, launch schedule and slice cap."""
+    rng = np.random.default_rng(90000 + i)
+    hkv = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+    group = int(rng.choice([1, 2, 4, 8, 16]))
+    batch = int(rng.integers(1, 600))
+    kind = i % 6
+    if kind == 0:
+        lens = rng.integers(0, 40, batch)
+    elif kind == 1:
+        lens = 16 * rng.integers(0, 200, batch) + rng.integers(-1, 2, batch)
+    elif kind == 2:
+        lens = np.where(rng.random(batch) < 0.05, rng.integers(2000, 12000, batch),
+                        rng.integers(0, 100, batch))
+    elif kind == 3:
+        lens = rng.integers(1, 5000, batch)
+    elif kind == 4:
+        lens = np.full(batch, int(rng.integers(1, 3000)))
+    else:
+        lens = rng.integers(0, 2, batch)
+    lens = np.clip(lens, 0, None)
+    while int(lens.sum()) * hkv * group > 6_000_000 and batch > 1:
+        batch = max(1, batch // 2)
+        lens = lens[:batch]
+    case = W.build_case(lens.tolist(), hkv * group, hkv, 128, 16, seed=91000 + i,
+                        poison=bool(i % 2), extra_table_cols=int(rng.integers(0, 3)))
+    variant = str(rng.choice(["mfma", "mfma", "valu"]))
+    schedule = str(rng.choice(["fused", "fused", "staged", "two_kernel"]))
+    slices = int(rng.choice([0, 0, 0, 1, 2, 5, 63, 200, 777, 1024, 2048, 4096]))
+    return case, variant, schedule, slices
+
+
+@pytest.mark.parametrize("i", range(60))
+def test_mixed_random_shapes_and_launches(i):
+    case, variant, schedule, slices = mixed_random_case(i)
+    say(f"[mixed] case {i}: B={case.batch} Hq={case.num_q_heads} Hkv={case.num_kv_heads} "
+        f"sumL={case.total_tokens()} {variant} {schedule} slices={slices}")
+    ref = oracle.decode_attention(case)
+    assert_parity(run(case, variant=variant, schedule=schedule, max_slices=slices), ref,
+                  f"mixed random {i}")
+
+
 def large_random_case(i):
     rng = np.random.default_rng(5000 + i)
     hkv = int(rng.choice([1, 2, 4, 8]))
