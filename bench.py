@@ -642,6 +642,10 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--kv-layout", default="interleaved", choices=["interleaved", "separate"],
+                    help="interleaved: K and V caches in one allocation, each block's K and V "
+                         "adjacent (block stride 2 x num_kv_heads x 4 KiB); separate: two dense "
+                         "caches")
     ap.add_argument("--no-flush-pass", action="store_true",
                     help="skip the per-call pass with a 1 GiB read before each call")
     ap.add_argument("--seed", type=int, default=None)
@@ -701,7 +705,19 @@ def main(argv=None):
     # At least two copies of the cache, rotated, and at least 4x the Infinity
     # Cache in total: no step finds the tiles of the step before it there.
     nrep = max(2, math.ceil(4 * MALL_BYTES / kv_bytes))
-    reps = [(k, v)] + [(k.clone(), v.clone()) for _ in range(nrep - 1)]
+    if args.kv_layout == "interleaved":
+        # Each copy one allocation, each block's K and V in one run (new_kv_cache).
+        reps = []
+        for _ in range(nrep):
+            kk, vv = neo.new_kv_cache(case.num_blocks, case.num_kv_heads)
+            kk.copy_(k)
+            vv.copy_(v)
+            reps.append((kk, vv))
+        del k, v
+        torch.cuda.empty_cache()
+    else:
+        reps = [(k, v)] + [(k.clone(), v.clone()) for _ in range(nrep - 1)]
+    kv_stride = reps[0][0].stride(0)
     out = torch.empty((case.batch, case.num_q_heads, case.head_dim), dtype=torch.float32,
                       device="cuda")
     ws = neo.new_workspace(case.batch, case.num_q_heads, case.num_kv_heads)
@@ -722,12 +738,13 @@ def main(argv=None):
             case.num_q_heads, case.num_kv_heads, case.head_dim, case.block_size,
             float(case.scale), out.data_ptr(), case.batch, case.max_blocks_per_seq,
             case.num_blocks, ws.data_ptr(), ws.numel(), variant_id, schedule_id,
-            args.max_slices, evs[0], evs[1], sh)
+            args.max_slices, kv_stride, evs[0], evs[1], sh)
         if rc != 0:
             raise neo.NeoError(rc, lib.neo_last_error().decode())
 
     log(f"[bench] {case.name}: B={case.batch} sumL={case.total_tokens()} "
-        f"KV={kv_bytes / 1e6:.1f} MB x{nrep} replicas; warmup {args.warmup}")
+        f"KV={kv_bytes / 1e6:.1f} MB x{nrep} replicas, {args.kv_layout} layout; "
+        f"warmup {args.warmup}")
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -808,6 +825,8 @@ def main(argv=None):
             "num_kv_heads": case.num_kv_heads, "head_dim": case.head_dim,
             "block_size": case.block_size, "sum_seq_len": case.total_tokens(),
             "algorithmic_bytes_per_step": alg_bytes, "kv_replicas": nrep,
+            "kv_layout": (f"{args.kv_layout}: block stride {kv_stride} elements "
+                          f"({'K and V of a block in one run' if args.kv_layout == 'interleaved' else 'two dense caches'})"),
             "variant": resolved, "schedule": schedule, "max_slices": args.max_slices,
             "parallelism": "single GPU",
         },

@@ -13,6 +13,10 @@ heads in groups. Layouts (torch tensors, all on one GPU):
 * ``q``           bf16  ``[batch, num_q_heads, 128]``
 * ``k_cache``     bf16  ``[num_blocks, num_kv_heads, 16, 16, 8]``  (piece-major keys)
 * ``v_cache``     bf16  ``[num_blocks, num_kv_heads, 128, 16]``    (dim-major values)
+
+  dense within each block; the blocks themselves may be strided (the same stride
+  in both caches): ``new_kv_cache`` returns both as views of one allocation with
+  each block's K and V adjacent, the fastest layout measured on MI355X.
 * ``block_table`` int32 ``[batch, max_blocks_per_seq]``
 * ``seq_lens``    int32 ``[batch]``
 * result          fp32  ``[batch, num_q_heads, 128]``
@@ -29,7 +33,7 @@ __all__ = [
     "library_path", "load_library", "VARIANTS", "SCHEDULES", "MAX_SLICES", "version",
     "new_workspace", "kv_append", "copy_blocks", "cpu_decode_attention", "CPU_ISAS",
     "cpu_best_isa", "cpu_default_threads", "cpu_read_probe", "cpu_kv_append",
-    "read_probe", "read_probe_tiles", "READ_PROBE_SINK_WORDS",
+    "read_probe", "read_probe_tiles", "READ_PROBE_SINK_WORDS", "new_kv_cache",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -83,21 +87,22 @@ def load_library():
         lib.neo_decode_workspace_bytes.restype = ctypes.c_int
         lib.neo_decode_attention.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S, P]
         lib.neo_decode_attention.restype = ctypes.c_int
+        L = ctypes.c_int64
         lib.neo_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P, S,
-                                                I, I, I, P]
+                                                I, I, I, L, P]
         lib.neo_decode_attention_ex.restype = ctypes.c_int
         lib.neo_decode_attention_events.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P,
-                                                    S, I, I, I, P, P, P]
+                                                    S, I, I, I, L, P, P, P]
         lib.neo_decode_attention_events.restype = ctypes.c_int
         lib.neo_decode_attention_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P]
         lib.neo_decode_attention_noalloc.restype = ctypes.c_int
         lib.neo_decode_workspace_init.argtypes = [P, S, P]
         lib.neo_decode_workspace_init.restype = ctypes.c_int
-        lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, P, P]
+        lib.neo_paged_gather.argtypes = [P, I, P, P, P, I, I, I, I, I, I, L, P, P]
         lib.neo_paged_gather.restype = ctypes.c_int
-        lib.neo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
+        lib.neo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, L, P]
         lib.neo_kv_append.restype = ctypes.c_int
-        lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, P]
+        lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, L, L, P]
         lib.neo_read_probe.argtypes = [P, S, I, P, S, P]
         lib.neo_read_probe.restype = ctypes.c_int
         lib.neo_read_probe_tiles.argtypes = [P, S, I, I, P, S, P]
@@ -162,6 +167,43 @@ def _require(t, name, dtype, ndim):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _require_cache(t, name, ndim, *, pinned_ok=False):
+    """A bf16 GPU cache tensor (or, with ``pinned_ok``, one in pinned host
+    memory) whose blocks (dim 0) may be strided: every dim but the first dense,
+    the block stride a multiple of 8 elements of at least one block. Returns the
+    block stride in elements."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda" and not (pinned_ok and t.is_pinned()):
+        where = "on a GPU or in pinned host memory" if pinned_ok else "on a GPU"
+        raise ValueError(f"{name} must be {where} (got {t.device}); there is no CPU path")
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be torch.bfloat16 (got {t.dtype})")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims (got shape {tuple(t.shape)})")
+    inner = math.prod(t.shape[1:])
+    want = [math.prod(t.shape[d + 1:]) for d in range(1, ndim)]
+    if list(t.stride()[1:]) != want or t.stride(0) < inner or t.stride(0) % 8 != 0:
+        raise ValueError(f"{name} must be dense within each block, with a block stride that is "
+                         f"a multiple of 8 elements of at least {inner} (strides {t.stride()})")
+    return int(t.stride(0))
+
+
+def new_kv_cache(num_blocks: int, num_kv_heads: int, device="cuda", head_dim: int = 128,
+                 block_size: int = 16):
+    """(k_cache, v_cache) views of one allocation ``[num_blocks][K, V][num_kv_heads][tile]``:
+    each block's K and V in one run, the caches' block stride twice a block. Shapes as the
+    dense caches (``[NB, Hkv, 16, 16, 8]`` and ``[NB, Hkv, 128, 16]``); ``decode_attention``
+    reads the stride from them. Uninitialised."""
+    torch = _torch()
+    tile = head_dim * block_size
+    buf = torch.empty((num_blocks, 2, num_kv_heads, tile), dtype=torch.bfloat16, device=device)
+    k = buf[:, 0].view(num_blocks, num_kv_heads, head_dim // 8, block_size, 8)
+    v = buf[:, 1].view(num_blocks, num_kv_heads, head_dim, block_size)
+    return k, v
+
+
 def _stream_of(stream, device):
     torch = _torch()
     return torch.cuda.current_stream(device) if stream is None else stream
@@ -224,8 +266,7 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
     torch = _torch()
     lib = load_library()
     _require(q, "q", torch.bfloat16, 3)
-    _require(k_cache, "k_cache", torch.bfloat16, 5)
-    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    k_stride = _shared_stride(k_cache, "k_cache", v_cache, "v_cache")
     _require(block_table, "block_table", torch.int32, 2)
     _require(seq_lens, "seq_lens", torch.int32, 1)
     B, Hq, D = q.shape
@@ -266,7 +307,7 @@ def decode_attention(q, k_cache, v_cache, block_table, seq_lens, scale=None, out
             q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
             seq_lens.data_ptr(), Hq, Hkv, D, bs, float(scale), out.data_ptr(), B,
             block_table.shape[1], NB, workspace.data_ptr(), workspace.numel(),
-            VARIANTS[variant], SCHEDULES[schedule], int(max_slices), sh))
+            VARIANTS[variant], SCHEDULES[schedule], int(max_slices), k_stride, sh))
     return out
 
 
@@ -275,11 +316,11 @@ def paged_gather(cache, kind: str, block_table, seq_lens, *, token_offsets=None,
     torch = _torch()
     lib = load_library()
     if kind == "k":
-        _require(cache, "cache", torch.bfloat16, 5)
+        stride = _require_cache(cache, "cache", 5)
         NB, Hkv, npieces, bs, x = cache.shape
         D = npieces * x
     elif kind == "v":
-        _require(cache, "cache", torch.bfloat16, 4)
+        stride = _require_cache(cache, "cache", 4)
         NB, Hkv, D, bs = cache.shape
     else:
         raise ValueError("kind must be 'k' or 'v'")
@@ -299,7 +340,7 @@ def paged_gather(cache, kind: str, block_table, seq_lens, *, token_offsets=None,
         _check(lib.neo_paged_gather(cache.data_ptr(), 1 if kind == "v" else 0,
                                     block_table.data_ptr(), seq_lens.data_ptr(),
                                     token_offsets.data_ptr(), B, block_table.shape[1], Hkv, D,
-                                    bs, NB, dst.data_ptr(), sh))
+                                    bs, NB, stride, dst.data_ptr(), sh))
     return dst
 
 
@@ -322,11 +363,11 @@ def debug_validate(block_table, seq_lens, num_blocks: int, block_size: int = 16,
 
 def kv_append(k_cache, v_cache, k_new, v_new, block_table, seq_lens, *, stream=None):
     """Write each request's newest token (k_new, v_new: bf16 [B, Hkv, 128]) into the
-    paged caches at token seq_lens[b] - 1 (in place, on ``stream``)."""
+    paged caches at token seq_lens[b] - 1 (in place, on ``stream``). The caches may
+    be dense or share one block stride (``new_kv_cache``)."""
     torch = _torch()
     lib = load_library()
-    _require(k_cache, "k_cache", torch.bfloat16, 5)
-    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    stride = _shared_stride(k_cache, "k_cache", v_cache, "v_cache")
     _require(k_new, "k_new", torch.bfloat16, 3)
     _require(v_new, "v_new", torch.bfloat16, 3)
     _require(block_table, "block_table", torch.int32, 2)
@@ -339,30 +380,29 @@ def kv_append(k_cache, v_cache, k_new, v_new, block_table, seq_lens, *, stream=N
     with torch.cuda.device(k_cache.device):
         _check(lib.neo_kv_append(k_cache.data_ptr(), v_cache.data_ptr(), k_new.data_ptr(),
                                  v_new.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
-                                 B, block_table.shape[1], Hkv, npieces * x, bs, NB, sh))
+                                 B, block_table.shape[1], Hkv, npieces * x, bs, NB, stride,
+                                 sh))
 
 
-def _cache_arg(t, name, ndim):
-    """A cache tensor on the GPU or in pinned host memory (device-addressable)."""
-    torch = _torch()
-    if not isinstance(t, torch.Tensor) or t.dtype != torch.bfloat16 or t.dim() != ndim:
-        raise TypeError(f"{name} must be a bf16 tensor with {ndim} dims")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
-    if t.device.type != "cuda" and not t.is_pinned():
-        raise ValueError(f"{name} must be on a GPU or in pinned host memory")
+def _shared_stride(k, k_name, v, v_name, *, pinned_ok=False):
+    """Block stride of a K and V cache pair (both must have the same one)."""
+    ks = _require_cache(k, k_name, 5, pinned_ok=pinned_ok)
+    vs = _require_cache(v, v_name, 4, pinned_ok=pinned_ok)
+    if ks != vs:
+        raise ValueError(f"{k_name} and {v_name} must share one block stride ({ks} != {vs})")
+    return ks
 
 
 def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, *, stream=None, device=None):
     """dst block dst_ids[i] <- src block src_ids[i] for K and V. Caches may be GPU
-    tensors or pinned host tensors (``pin_memory=True``); ids are int32 GPU
-    tensors. Runs as one kernel on ``stream`` (of ``device``, default: the ids')."""
+    tensors or pinned host tensors (``pin_memory=True``), dense or with a block
+    stride shared by the pair (source and destination strides may differ); ids
+    are int32 GPU tensors. Runs as one kernel on ``stream`` (of ``device``,
+    default: the ids')."""
     torch = _torch()
     lib = load_library()
-    _cache_arg(src_k, "src_k", 5)
-    _cache_arg(dst_k, "dst_k", 5)
-    _cache_arg(src_v, "src_v", 4)
-    _cache_arg(dst_v, "dst_v", 4)
+    src_stride = _shared_stride(src_k, "src_k", src_v, "src_v", pinned_ok=True)
+    dst_stride = _shared_stride(dst_k, "dst_k", dst_v, "dst_v", pinned_ok=True)
     _require(src_ids, "src_ids", torch.int32, 1)
     _require(dst_ids, "dst_ids", torch.int32, 1)
     if src_ids.shape != dst_ids.shape:
@@ -376,7 +416,7 @@ def copy_blocks(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, *, stream=None, de
         _check(lib.neo_kv_copy_blocks(src_k.data_ptr(), src_v.data_ptr(), dst_k.data_ptr(),
                                       dst_v.data_ptr(), src_ids.data_ptr(), dst_ids.data_ptr(),
                                       src_ids.shape[0], Hkv, npieces * x, bs, NB_s,
-                                      dst_k.shape[0], sh))
+                                      dst_k.shape[0], src_stride, dst_stride, sh))
 
 
 def read_probe(src, sink, *, nontemporal: bool = True, stream=None):

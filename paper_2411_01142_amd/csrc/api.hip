@@ -105,6 +105,23 @@ neo_status check_heads(int32_t hq, int32_t hkv, int32_t head_dim) {
   return NEO_OK;
 }
 
+// A cache's block stride in elements: 0 stands for `dense` (num_kv_heads tiles,
+// blocks back to back); otherwise a multiple of 8 (whole 16-byte words) of at
+// least `dense` -- the stride may leave room after a block (the other cache's
+// block, padding) but not less -- and at most 2^40, so that block id * stride
+// stays far inside 64 bits. *resolved gets the stride to use.
+neo_status check_block_stride(int64_t stride, int64_t dense, const char* name,
+                              int64_t* resolved) {
+  if (stride != 0 &&
+      (stride < dense || stride % neo::kPiece != 0 || stride > ((int64_t)1 << 40)))
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "%s %lld must be 0 or a multiple of %d of at least %lld elements "
+                     "(and at most 2^40)",
+                     name, (long long)stride, neo::kPiece, (long long)dense);
+  *resolved = stride != 0 ? stride : dense;
+  return NEO_OK;
+}
+
 // Host-side checks of a decode call, shared by every decode entry point (no
 // HIP call). *noop is set for an empty batch, which needs no pointer.
 neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
@@ -112,7 +129,8 @@ neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
                         int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                         int32_t block_size, float scale, const float* out, int32_t batch,
                         int32_t max_blocks_per_seq, int32_t num_blocks, int32_t variant,
-                        int32_t schedule, int32_t max_slices, bool* noop) {
+                        int32_t schedule, int32_t max_slices, int64_t kv_block_stride,
+                        bool* noop) {
   *noop = false;
   if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   const neo_status st = check_heads(num_q_heads, num_kv_heads, head_dim);
@@ -129,6 +147,10 @@ neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
   if (max_slices < 0 || max_slices > NEO_MAX_SLICES)
     return set_error(NEO_ERR_INVALID_ARG, "max_slices %d outside [0, %d]", max_slices,
                      NEO_MAX_SLICES);
+  int64_t resolved = 0;
+  const neo_status sst = check_block_stride(kv_block_stride, (int64_t)num_kv_heads * neo::kTileElems,
+                                            "kv_block_stride", &resolved);
+  if (sst != NEO_OK) return sst;
   if (batch == 0) {
     *noop = true;
     return ok();
@@ -232,13 +254,13 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
                                        int32_t num_blocks, void* workspace,
                                        size_t workspace_bytes, int32_t variant,
                                        int32_t schedule, int32_t max_slices,
-                                       void* decode_start_event, void* decode_end_event,
-                                       void* stream) {
+                                       int64_t kv_block_stride, void* decode_start_event,
+                                       void* decode_end_event, void* stream) {
   bool noop = false;
   neo_status st = check_decode(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                num_kv_heads, head_dim, block_size, scale, out, batch,
                                max_blocks_per_seq, num_blocks, variant, schedule, max_slices,
-                               &noop);
+                               kv_block_stride, &noop);
   if (st != NEO_OK || noop) return st;
   const int32_t group = num_q_heads / num_kv_heads;
   const neo::WorkspaceLayout wl = neo::workspace_layout(batch, group);
@@ -289,6 +311,7 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
   p.slice_quantum = quantum;
   p.xcd8 = xcds == 8;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.blk_stride = kv_block_stride != 0 ? kv_block_stride : (int64_t)num_kv_heads * neo::kTileElems;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
@@ -324,11 +347,13 @@ neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const voi
                                    int32_t block_size, float scale, float* out, int32_t batch,
                                    int32_t max_blocks_per_seq, int32_t num_blocks,
                                    void* workspace, size_t workspace_bytes, int32_t variant,
-                                   int32_t schedule, int32_t max_slices, void* stream) {
+                                   int32_t schedule, int32_t max_slices, int64_t kv_block_stride,
+                                   void* stream) {
   return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                      num_kv_heads, head_dim, block_size, scale, out, batch,
                                      max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
-                                     variant, schedule, max_slices, nullptr, nullptr, stream);
+                                     variant, schedule, max_slices, kv_block_stride, nullptr,
+                                     nullptr, stream);
 }
 
 neo_status neo_decode_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -340,7 +365,7 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
   return neo_decode_attention_events(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                      num_kv_heads, head_dim, block_size, scale, out, batch,
                                      max_blocks_per_seq, num_blocks, workspace, workspace_bytes,
-                                     NEO_VARIANT_AUTO, NEO_SCHEDULE_AUTO, 0, nullptr, nullptr,
+                                     NEO_VARIANT_AUTO, NEO_SCHEDULE_AUTO, 0, 0, nullptr, nullptr,
                                      stream);
 }
 
@@ -354,7 +379,7 @@ neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, cons
   neo_status st = check_decode(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                num_kv_heads, head_dim, block_size, scale, out, batch,
                                max_blocks_per_seq, num_blocks, NEO_VARIANT_AUTO,
-                               NEO_SCHEDULE_AUTO, 0, &noop);
+                               NEO_SCHEDULE_AUTO, 0, 0, &noop);
   if (st != NEO_OK || noop) return st;
   const int32_t group = num_q_heads / num_kv_heads;
   if (group > kScratchMaxGroup)
@@ -393,6 +418,7 @@ neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, cons
   p.slice_quantum = quantum;
   p.xcd8 = xcds == 8;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.blk_stride = (int64_t)num_kv_heads * neo::kTileElems;
   const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
   const hipError_t e = neo::launch_decode_mfma(p, group, neo::kFused, grid, s);
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
@@ -412,12 +438,18 @@ neo_status neo_decode_workspace_init(void* workspace, size_t workspace_bytes, vo
 neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* block_table,
                             const int32_t* seq_lens, const int32_t* token_offsets, int32_t batch,
                             int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
-                            int32_t block_size, int32_t num_blocks, void* dst, void* stream) {
+                            int32_t block_size, int32_t num_blocks, int64_t block_stride,
+                            void* dst, void* stream) {
   if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   if (is_v != 0 && is_v != 1) return set_error(NEO_ERR_INVALID_ARG, "is_v must be 0 or 1");
-  if (num_kv_heads <= 0 || head_dim <= 0 || head_dim % neo::kPiece != 0 || block_size <= 0)
+  if (num_kv_heads <= 0 || head_dim <= 0 || head_dim % neo::kPiece != 0 || block_size <= 0 ||
+      (int64_t)num_kv_heads * head_dim * block_size >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG, "bad shape (num_kv_heads %d, head_dim %d, block_size %d)",
                      num_kv_heads, head_dim, block_size);
+  int64_t stride = 0;
+  const neo_status sst = check_block_stride(
+      block_stride, (int64_t)num_kv_heads * head_dim * block_size, "block_stride", &stride);
+  if (sst != NEO_OK) return sst;
   if (batch == 0) return ok();
   if (!cache || !block_table || !seq_lens || !token_offsets || !dst)
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
@@ -428,7 +460,7 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   hipError_t e = neo::launch_gather(static_cast<const uint16_t*>(cache), is_v, block_table,
                                     seq_lens, token_offsets, batch, max_blocks_per_seq,
-                                    num_kv_heads, head_dim, block_size, num_blocks,
+                                    num_kv_heads, head_dim, block_size, num_blocks, stride,
                                     static_cast<uint16_t*>(dst), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "gather launch: %s", hipGetErrorString(e));
   return ok();
@@ -437,12 +469,17 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
 neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
                          const int32_t* block_table, const int32_t* seq_lens, int32_t batch,
                          int32_t max_blocks_per_seq, int32_t num_kv_heads, int32_t head_dim,
-                         int32_t block_size, int32_t num_blocks, void* stream) {
+                         int32_t block_size, int32_t num_blocks, int64_t kv_block_stride,
+                         void* stream) {
   if (batch < 0) return set_error(NEO_ERR_INVALID_ARG, "batch (%d) is negative", batch);
   if (num_kv_heads <= 0) return set_error(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
   if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
     return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
                      head_dim, block_size);
+  int64_t stride = 0;
+  const neo_status sst = check_block_stride(
+      kv_block_stride, (int64_t)num_kv_heads * neo::kTileElems, "kv_block_stride", &stride);
+  if (sst != NEO_OK) return sst;
   if (batch == 0) return ok();
   if (!k_cache || !v_cache || !k_new || !v_new || !block_table || !seq_lens)
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
@@ -457,7 +494,7 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
   hipError_t e = neo::launch_kv_append(
       static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
       static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), block_table,
-      seq_lens, batch, max_blocks_per_seq, num_kv_heads, num_blocks,
+      seq_lens, batch, max_blocks_per_seq, num_kv_heads, num_blocks, stride,
       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "append launch: %s", hipGetErrorString(e));
   return ok();
@@ -466,12 +503,19 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
 neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                               const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
                               int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
-                              int32_t src_num_blocks, int32_t dst_num_blocks, void* stream) {
+                              int32_t src_num_blocks, int32_t dst_num_blocks,
+                              int64_t src_block_stride, int64_t dst_block_stride, void* stream) {
   if (n < 0) return set_error(NEO_ERR_INVALID_ARG, "n (%d) is negative", n);
   if (num_kv_heads <= 0) return set_error(NEO_ERR_INVALID_ARG, "num_kv_heads must be positive");
   if (head_dim != neo::kHeadDim || block_size != neo::kBlock)
     return set_error(NEO_ERR_UNSUPPORTED, "head_dim %d / block_size %d unsupported (128 / 16)",
                      head_dim, block_size);
+  const int64_t dense = (int64_t)num_kv_heads * neo::kTileElems;
+  int64_t src_stride = 0, dst_stride = 0;
+  neo_status sst = check_block_stride(src_block_stride, dense, "src_block_stride", &src_stride);
+  if (sst != NEO_OK) return sst;
+  sst = check_block_stride(dst_block_stride, dense, "dst_block_stride", &dst_stride);
+  if (sst != NEO_OK) return sst;
   if (n == 0) return ok();
   if (!src_k || !src_v || !dst_k || !dst_v || !src_ids || !dst_ids)
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
@@ -496,7 +540,8 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
       static_cast<const uint16_t*>(dev[0]), static_cast<const uint16_t*>(dev[1]),
       static_cast<uint16_t*>(dev[2]), static_cast<uint16_t*>(dev[3]),
       static_cast<const int32_t*>(dev[4]), static_cast<const int32_t*>(dev[5]), n, num_kv_heads,
-      src_num_blocks, dst_num_blocks, in_hbm[2] && in_hbm[3], static_cast<hipStream_t>(stream));
+      src_num_blocks, dst_num_blocks, src_stride, dst_stride, in_hbm[2] && in_hbm[3],
+      static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
   return ok();
 }

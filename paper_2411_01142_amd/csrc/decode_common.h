@@ -647,7 +647,7 @@ __device__ inline void decode_driver(const DecodeParams& p) {
 
   __shared__ typename F::Shared shared[kWavesPerGroup];
   typename F::Shared& sh = shared[wv];
-  const size_t blk_stride = (size_t)p.hkv * kTileElems;
+  const size_t blk_stride = (size_t)p.blk_stride;
 
   // A slice holds at most two cut pairs: the one it starts in and the one it
   // ends in. Their merges (fused launch) run after the tile loop. Two named

@@ -9,13 +9,15 @@ namespace neo {
 hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new,
                             const uint16_t* v_new, const int32_t* table, const int32_t* lens,
                             int32_t batch, int32_t mbps, int32_t hkv, int32_t num_blocks,
-                            hipStream_t stream);
-// dst_in_hbm: the destination caches are device memory (streaming stores pay
-// there; into pinned host memory over the link they measured slightly slower).
+                            int64_t blk_stride, hipStream_t stream);
+// Block strides in elements, multiples of 8. dst_in_hbm: the destination
+// caches are device memory (streaming stores pay there; into pinned host
+// memory over the link they measured slightly slower).
 hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
                               uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
                               int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
-                              bool dst_in_hbm, hipStream_t stream);
+                              int64_t src_stride, int64_t dst_stride, bool dst_in_hbm,
+                              hipStream_t stream);
 
 // Streaming-read probe: reads n16 16-byte words once; sink gets one word per
 // wave (kReadProbeWaves of them), the xor of every 32-bit word that wave read.

@@ -18,11 +18,12 @@ namespace {
 // One workgroup of 128 threads per (request, kv head): thread d writes dim d
 // of the value row (a 2-byte store: V is dim-major, so the token's dims are
 // 32 bytes apart), threads 0-15 also write one 16-byte key piece each.
+// blk_stride: elements from one block of a cache to the next.
 __global__ __launch_bounds__(128) void append_kernel(
     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
     const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
     const int32_t* __restrict__ table, const int32_t* __restrict__ lens, int32_t mbps,
-    int32_t hkv, int32_t num_blocks) {
+    int32_t hkv, int32_t num_blocks, int64_t blk_stride) {
   const int b = blockIdx.x / hkv, g = blockIdx.x % hkv;
   const int32_t L = clamp_len(lens[b], mbps);
   if (L <= 0) return;
@@ -30,7 +31,7 @@ __global__ __launch_bounds__(128) void append_kernel(
   const int32_t blk = table[(size_t)b * mbps + t / kBlock];
   if (blk < 0 || blk >= num_blocks) return;
   const int slot = t % kBlock;
-  const size_t tile = ((size_t)blk * hkv + g) * kTileElems;
+  const size_t tile = (size_t)blk * (size_t)blk_stride + (size_t)g * kTileElems;
   const size_t src = ((size_t)b * hkv + g) * kHeadDim;
   const int d = threadIdx.x;
   if (d < kHeadDim / kPiece) {
@@ -51,17 +52,19 @@ __global__ __launch_bounds__(256) void copy_blocks_kernel(
     const uint16_t* __restrict__ src_k, const uint16_t* __restrict__ src_v,
     uint16_t* __restrict__ dst_k, uint16_t* __restrict__ dst_v,
     const int32_t* __restrict__ src_ids, const int32_t* __restrict__ dst_ids, int32_t hkv,
-    int32_t src_blocks, int32_t dst_blocks) {
+    int32_t src_blocks, int32_t dst_blocks, int64_t src_stride, int64_t dst_stride) {
   constexpr int kUnroll = 4;
   const int i = blockIdx.x;
   const int32_t s = src_ids[i], d = dst_ids[i];
   if (s < 0 || s >= src_blocks || d < 0 || d >= dst_blocks) return;
-  // 16-byte words per block per cache: hkv * 256, a multiple of blockDim.
+  // 16-byte words per block per cache: hkv * 256, a multiple of blockDim. The
+  // block strides (elements) are multiples of 8, i.e. whole 16-byte words.
   const int words = hkv * (kTileElems / 8);
-  const u32x4_t* sk = reinterpret_cast<const u32x4_t*>(src_k) + (size_t)s * words;
-  const u32x4_t* sv = reinterpret_cast<const u32x4_t*>(src_v) + (size_t)s * words;
-  u32x4_t* dk = reinterpret_cast<u32x4_t*>(dst_k) + (size_t)d * words;
-  u32x4_t* dv = reinterpret_cast<u32x4_t*>(dst_v) + (size_t)d * words;
+  const size_t so = (size_t)s * (size_t)(src_stride / 8), doff = (size_t)d * (size_t)(dst_stride / 8);
+  const u32x4_t* sk = reinterpret_cast<const u32x4_t*>(src_k) + so;
+  const u32x4_t* sv = reinterpret_cast<const u32x4_t*>(src_v) + so;
+  u32x4_t* dk = reinterpret_cast<u32x4_t*>(dst_k) + doff;
+  u32x4_t* dv = reinterpret_cast<u32x4_t*>(dst_v) + doff;
   for (int w0 = 0; w0 < words; w0 += kUnroll * 256) {
     // Rows of 256 words left in this step (fewer than kUnroll only at the end).
     const int rows = min(kUnroll, (words - w0) / 256);
@@ -95,22 +98,25 @@ __global__ __launch_bounds__(256) void copy_blocks_kernel(
 hipError_t launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new,
                             const uint16_t* v_new, const int32_t* table, const int32_t* lens,
                             int32_t batch, int32_t mbps, int32_t hkv, int32_t num_blocks,
-                            hipStream_t stream) {
-  append_kernel<<<(unsigned)batch * hkv, kHeadDim, 0, stream>>>(k_cache, v_cache, k_new, v_new,
-                                                               table, lens, mbps, hkv, num_blocks);
+                            int64_t blk_stride, hipStream_t stream) {
+  append_kernel<<<(unsigned)batch * hkv, kHeadDim, 0, stream>>>(
+      k_cache, v_cache, k_new, v_new, table, lens, mbps, hkv, num_blocks, blk_stride);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_blocks(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k,
                               uint16_t* dst_v, const int32_t* src_ids, const int32_t* dst_ids,
                               int32_t n, int32_t hkv, int32_t src_blocks, int32_t dst_blocks,
-                              bool dst_in_hbm, hipStream_t stream) {
+                              int64_t src_stride, int64_t dst_stride, bool dst_in_hbm,
+                              hipStream_t stream) {
   if (dst_in_hbm)
     copy_blocks_kernel<true><<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids, dst_ids,
-                                                    hkv, src_blocks, dst_blocks);
+                                                    hkv, src_blocks, dst_blocks, src_stride,
+                                                    dst_stride);
   else
     copy_blocks_kernel<false><<<n, 256, 0, stream>>>(src_k, src_v, dst_k, dst_v, src_ids,
-                                                     dst_ids, hkv, src_blocks, dst_blocks);
+                                                     dst_ids, hkv, src_blocks, dst_blocks,
+                                                     src_stride, dst_stride);
   return hipGetLastError();
 }
 

@@ -198,6 +198,7 @@ struct DecodeParams {
   int32_t slice_quantum;          // compute units x wavefronts per workgroup
   int32_t xcd8;                   // the device has eight XCDs (slice weights)
   float scale_log2;           // scale * log2(e)
+  int64_t blk_stride;         // elements from one block of a cache to the next (K and V alike)
 };
 
 // Launchers (each returns the hipError_t of its launch).
@@ -213,7 +214,8 @@ hipError_t launch_combine(const DecodeParams& p, int32_t group, int32_t grid, hi
 hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,
                          const int32_t* lens, const int32_t* offsets, int32_t batch,
                          int32_t mbps, int32_t hkv, int32_t head_dim, int32_t block_size,
-                         int32_t num_blocks, uint16_t* dst, hipStream_t stream);
+                         int32_t num_blocks, int64_t blk_stride, uint16_t* dst,
+                         hipStream_t stream);
 hipError_t launch_validate(const int32_t* table, const int32_t* lens, int32_t batch,
                            int32_t mbps, int32_t block_size, int32_t num_blocks,
                            int32_t* error_count, hipStream_t stream);

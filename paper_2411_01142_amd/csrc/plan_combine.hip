@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* __restrict__ d
 __global__ __launch_bounds__(256) void gather_kernel(
     const uint16_t* __restrict__ cache, int32_t is_v, const int32_t* __restrict__ table,
     const int32_t* __restrict__ lens, const int32_t* __restrict__ offsets, int32_t mbps,
-    int32_t hkv, int32_t head_dim, int32_t block_size, int32_t num_blocks,
+    int32_t hkv, int32_t head_dim, int32_t block_size, int32_t num_blocks, int64_t blk_stride,
     uint16_t* __restrict__ dst) {
   const int j = blockIdx.x, b = blockIdx.y;
   const int32_t L = min(max(lens[b], 0), mbps * block_size);
@@ -176,9 +176,10 @@ __global__ __launch_bounds__(256) void gather_kernel(
       const int d = c * kPiece + e;
       size_t src;
       if (is_v)
-        src = (((size_t)phys * hkv + g) * head_dim + d) * block_size + o;
+        src = ((size_t)g * head_dim + d) * block_size + o;
       else
-        src = ((((size_t)phys * hkv + g) * pieces + c) * block_size + o) * kPiece + e;
+        src = (((size_t)g * pieces + c) * block_size + o) * kPiece + e;
+      src += (size_t)phys * (size_t)blk_stride;
       vals[e] = cache[src];
     }
     uint16_t* out = dst + ((row0 + o) * hkv + g) * head_dim + c * kPiece;
@@ -239,9 +240,11 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
 hipError_t launch_gather(const uint16_t* cache, int32_t is_v, const int32_t* table,
                          const int32_t* lens, const int32_t* offsets, int32_t batch,
                          int32_t mbps, int32_t hkv, int32_t head_dim, int32_t block_size,
-                         int32_t num_blocks, uint16_t* dst, hipStream_t stream) {
+                         int32_t num_blocks, int64_t blk_stride, uint16_t* dst,
+                         hipStream_t stream) {
   gather_kernel<<<dim3(mbps, batch), 256, 0, stream>>>(cache, is_v, table, lens, offsets, mbps,
-                                                       hkv, head_dim, block_size, num_blocks, dst);
+                                                       hkv, head_dim, block_size, num_blocks,
+                                                       blk_stride, dst);
   return hipGetLastError();
 }
 

@@ -134,15 +134,32 @@ class Case:
         L = np.maximum(self.seq_lens.astype(np.int64), 0)
         return int(L.sum()) * self.num_q_heads * self.head_dim * 4
 
-    def to_torch(self, device="cuda"):
+    def to_torch(self, device="cuda", kv_layout: str = "separate", kv_pad: int = 0):
         """(q, k_cache, v_cache, block_table, seq_lens) as torch tensors on ``device``
-        (bf16 caches and q, int32 table and lengths)."""
+        (bf16 caches and q, int32 table and lengths).
+
+        ``kv_layout="separate"``: two dense caches. ``"interleaved"``: both caches
+        views of one buffer whose block b holds K's block then V's block, plus
+        ``kv_pad`` elements (a multiple of 8) after each; the caches' block stride
+        is then ``2 * Hkv * head_dim * block_size + kv_pad`` elements."""
         import torch
 
         def bf16(a):
             return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(
                 torch.bfloat16)
-        return (bf16(self.q), bf16(self.k_cache), bf16(self.v_cache),
+        k, v = bf16(self.k_cache), bf16(self.v_cache)
+        if kv_layout == "interleaved":
+            nb, per = self.num_blocks, self.num_kv_heads * self.head_dim * self.block_size
+            buf = torch.full((nb, 2 * per + kv_pad), float("nan"), dtype=torch.bfloat16,
+                             device=device)
+            kk = buf[:, :per].view(k.shape)
+            vv = buf[:, per:2 * per].view(v.shape)
+            kk.copy_(k)
+            vv.copy_(v)
+            k, v = kk, vv
+        elif kv_layout != "separate":
+            raise ValueError(f"unknown kv_layout {kv_layout!r}")
+        return (bf16(self.q), k, v,
                 torch.from_numpy(np.ascontiguousarray(self.block_table)).to(device),
                 torch.from_numpy(np.ascontiguousarray(self.seq_lens)).to(device))
 

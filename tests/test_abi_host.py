@@ -103,12 +103,13 @@ FAKE = 1 << 20  # non-null, 256-aligned host address; never dereferenced on thes
 def call(lib, **kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, table=FAKE, lens=FAKE, hq=32, hkv=8, d=128, bs=16,
              scale=1 / math.sqrt(128), out=FAKE, batch=4, mbps=8, nb=100, ws=FAKE,
-             ws_bytes=1 << 40, variant=0, schedule=0, slices=0, stream=None)
+             ws_bytes=1 << 40, variant=0, schedule=0, slices=0, kv_stride=0, stream=None)
     a.update(kw)
     return lib.neo_decode_attention_ex(a["q"], a["k"], a["v"], a["table"], a["lens"], a["hq"],
                                        a["hkv"], a["d"], a["bs"], a["scale"], a["out"],
                                        a["batch"], a["mbps"], a["nb"], a["ws"], a["ws_bytes"],
-                                       a["variant"], a["schedule"], a["slices"], a["stream"])
+                                       a["variant"], a["schedule"], a["slices"], a["kv_stride"],
+                                       a["stream"])
 
 
 @pytest.mark.parametrize("kw,code,needle", [
@@ -139,6 +140,10 @@ def call(lib, **kw):
     (dict(slices=100000), INVALID, "max_slices"),
     (dict(batch=1 << 20, mbps=1 << 12), INVALID, "2^31"),
     (dict(batch=1 << 18, mbps=(1 << 10) - 3), INVALID, "+ 3)"),
+    (dict(kv_stride=8 * 2048 - 8), INVALID, "kv_block_stride"),
+    (dict(kv_stride=2 * 8 * 2048 + 4), INVALID, "kv_block_stride"),
+    (dict(kv_stride=-2048), INVALID, "kv_block_stride"),
+    (dict(kv_stride=1 << 41), INVALID, "kv_block_stride"),
 ])
 def test_decode_rejects_bad_arguments_before_any_hip_call(lib, kw, code, needle):
     assert call(lib, **kw) == code
@@ -158,14 +163,19 @@ def test_plain_entry_point_validates_too(lib):
 
 
 def test_gather_and_validate_reject(lib):
-    assert lib.neo_paged_gather(FAKE, 2, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, FAKE,
+    assert lib.neo_paged_gather(FAKE, 2, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, 0, FAKE,
                                 None) == INVALID
-    assert lib.neo_paged_gather(FAKE, 0, FAKE, FAKE, FAKE, 4, 8, 8, 100, 16, 100, FAKE,
+    assert lib.neo_paged_gather(FAKE, 0, FAKE, FAKE, FAKE, 4, 8, 8, 100, 16, 100, 0, FAKE,
                                 None) == INVALID
-    assert lib.neo_paged_gather(None, 0, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, FAKE,
+    assert lib.neo_paged_gather(None, 0, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, 0, FAKE,
                                 None) == INVALID
-    assert lib.neo_paged_gather(None, 0, None, None, None, 0, 8, 8, 128, 16, 100, None,
+    assert lib.neo_paged_gather(None, 0, None, None, None, 0, 8, 8, 128, 16, 100, 0, None,
                                 None) == OK
+    # block strides below one block, not a multiple of 8, or beyond 2^40
+    for bad in (8 * 128 * 16 - 8, 8 * 128 * 16 + 4, (1 << 40) + 8, -8):
+        assert lib.neo_paged_gather(FAKE, 1, FAKE, FAKE, FAKE, 4, 8, 8, 128, 16, 100, bad, FAKE,
+                                    None) == INVALID
+        assert "block_stride" in lib.neo_last_error().decode()
     assert lib.neo_debug_validate(FAKE, FAKE, 4, 0, 16, 100, FAKE, None) == INVALID
     assert lib.neo_debug_validate(None, FAKE, 4, 8, 16, 100, FAKE, None) == INVALID
     assert lib.neo_decode_workspace_init(None, 1024, None) == INVALID
@@ -174,10 +184,10 @@ def test_gather_and_validate_reject(lib):
 
 def append_call(lib, **kw):
     a = dict(k=FAKE, v=FAKE, kn=FAKE, vn=FAKE, table=FAKE, lens=FAKE, batch=4, mbps=8, hkv=8,
-             d=128, bs=16, nb=100)
+             d=128, bs=16, nb=100, stride=0)
     a.update(kw)
     return lib.neo_kv_append(a["k"], a["v"], a["kn"], a["vn"], a["table"], a["lens"], a["batch"],
-                             a["mbps"], a["hkv"], a["d"], a["bs"], a["nb"], None)
+                             a["mbps"], a["hkv"], a["d"], a["bs"], a["nb"], a["stride"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -186,6 +196,8 @@ def append_call(lib, **kw):
     (dict(table=None), INVALID), (dict(mbps=0), INVALID), (dict(nb=0), INVALID),
     (dict(k=FAKE + 2), INVALID), (dict(kn=FAKE + 8), INVALID), (dict(v=FAKE + 1), INVALID),
     (dict(mbps=1 << 28), INVALID), (dict(batch=1 << 28, hkv=16), INVALID),
+    (dict(stride=8 * 2048 - 8), INVALID), (dict(stride=8 * 2048 + 2), INVALID),
+    (dict(stride=-1), INVALID),
 ])
 def test_kv_append_rejects(lib, kw, code):
     assert append_call(lib, **kw) == code
@@ -199,10 +211,11 @@ def test_kv_append_empty_batch_is_a_noop(lib):
 
 def copy_call(lib, **kw):
     a = dict(sk=FAKE, sv=FAKE, dk=FAKE, dv=FAKE, si=FAKE, di=FAKE, n=4, hkv=8, d=128, bs=16,
-             snb=100, dnb=100)
+             snb=100, dnb=100, sst=0, dst=0)
     a.update(kw)
     return lib.neo_kv_copy_blocks(a["sk"], a["sv"], a["dk"], a["dv"], a["si"], a["di"], a["n"],
-                                  a["hkv"], a["d"], a["bs"], a["snb"], a["dnb"], None)
+                                  a["hkv"], a["d"], a["bs"], a["snb"], a["dnb"], a["sst"],
+                                  a["dst"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -210,6 +223,8 @@ def copy_call(lib, **kw):
     (dict(bs=32), UNSUPPORTED), (dict(sk=None), INVALID), (dict(dv=None), INVALID),
     (dict(di=None), INVALID), (dict(snb=0), INVALID), (dict(dnb=-5), INVALID),
     (dict(sv=FAKE + 8), INVALID), (dict(dk=FAKE + 4), INVALID),
+    (dict(sst=8 * 2048 - 8), INVALID), (dict(dst=2 * 8 * 2048 + 6), INVALID),
+    (dict(dst=(1 << 40) + 8), INVALID),
 ])
 def test_kv_copy_blocks_rejects(lib, kw, code):
     assert copy_call(lib, **kw) == code

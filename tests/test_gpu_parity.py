@@ -39,8 +39,8 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run(case, **kw):
-    q, k, v, bt, sl = case.to_torch("cuda")
+def run(case, kv_layout="separate", kv_pad=0, **kw):
+    q, k, v, bt, sl = case.to_torch("cuda", kv_layout=kv_layout, kv_pad=kv_pad)
     out = neo.decode_attention(q, k, v, bt, sl, scale=case.scale, **kw)
     torch.cuda.synchronize()
     return out.cpu().numpy()
@@ -156,6 +156,50 @@ def test_config_parity(cfg, seed):
     ae, re = assert_parity(y, ref, f"{case.name} (all {case.batch * case.num_q_heads} rows)")
     record(f"{case.name}: all {case.batch * case.num_q_heads} rows, max_abs={ae:.2e} "
            f"max_rel_rownorm={re:.2e}")
+
+
+# --------------------------------------------------------------------- block stride
+
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5, 6])
+def test_interleaved_caches_full_size(cfg):
+    # Both caches in one allocation, each block's K then V (the layout the
+    # benchmark uses): every row against the oracle, and the same bits as two
+    # dense caches (only the addresses differ).
+    case = W.make_config(cfg, cfg)
+    say(f"[layout] {case.name}: interleaved caches")
+    a = run(case, kv_layout="interleaved")
+    ae, re = assert_parity(a, oracle.decode_attention(case), f"{case.name} interleaved")
+    record(f"{case.name}, K and V of each block in one run: max_abs={ae:.2e} "
+           f"max_rel_rownorm={re:.2e}")
+    assert np.array_equal(a, run(case))
+
+
+@pytest.mark.parametrize("pad", [8, 2048, 12288 + 8])
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("schedule", ["fused", "staged", "two_kernel"])
+def test_block_stride_with_padding(pad, variant, schedule):
+    # Strides that are not twice a block (padding after each block's K and V,
+    # NaN-filled, never read), on every kernel family and launch.
+    case = W.build_case([1, 15, 16, 17, 300, 1000, 0, 2500], 32, 8, 128, 16, seed=61)
+    ref = oracle.decode_attention(case)
+    a = run(case, kv_layout="interleaved", kv_pad=pad, variant=variant, schedule=schedule,
+            max_slices=0 if schedule == "fused" else 97)
+    assert_parity(a, ref, f"stride pad {pad} {variant} {schedule}")
+    assert np.array_equal(a, run(case, variant=variant, schedule=schedule,
+                                 max_slices=0 if schedule == "fused" else 97))
+
+
+def test_binding_checks_cache_strides():
+    case = W.build_case([10, 40], 8, 2, 128, 16, seed=62)
+    q, k, v, bt, sl = case.to_torch("cuda", kv_layout="interleaved")
+    with pytest.raises(ValueError, match="block stride"):
+        neo.decode_attention(q, k, v.contiguous(), bt, sl)      # strides differ
+    kt = k.transpose(3, 4)                                       # not dense within a block
+    with pytest.raises(ValueError, match="dense"):
+        neo.decode_attention(q, kt, v, bt, sl)
+    kk, vv = neo.new_kv_cache(case.num_blocks, case.num_kv_heads)
+    assert kk.stride(0) == vv.stride(0) == 2 * case.num_kv_heads * 2048
+    assert vv.data_ptr() - kk.data_ptr() == case.num_kv_heads * 2048 * 2
 
 
 # --------------------------------------------------------------------- edge cases
