@@ -316,14 +316,32 @@ def bench_read_ceiling(args, torch, neo):
     buffer), nontemporal and plain loads; and the tile probe, the decode
     kernel's own pattern without its arithmetic (contiguous 8 KiB steps per
     wave through 4 KiB buffer resources, nontemporal), over a sweep of waves per
-    compute unit and steps in flight. The best median is the measured read
-    ceiling."""
+    compute unit and steps in flight. Each configuration is timed two ways: its
+    calls back to back between two events (as the decode benchmark's timed
+    region runs), and one call at a time with the device idle in between (the
+    median of those). The best back-to-back rate is the measured read ceiling:
+    the one-at-a-time intervals also hold the dispatch latency of a kernel
+    launched onto an idle stream (25-30 us), which back-to-back calls hide."""
     nbytes = 4 << 30
     src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
     sink = torch.empty(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
     hip = HipEvents()
     sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     reps = max(args.steps // 10, 5)
+
+    def back_to_back(fn):
+        for _ in range(2):
+            fn()
+        a, b = hip.create(), hip.create()
+        hip.record(a, sh)
+        for _ in range(2 * reps):
+            fn()
+        hip.record(b, sh)
+        torch.cuda.synchronize()
+        ms = hip.elapsed_ms(a, b) / (2 * reps)
+        hip.destroy(a)
+        hip.destroy(b)
+        return round(nbytes / (ms * 1e-3) / 1e9, 1)
 
     def rate(fn):
         for _ in range(2):
@@ -339,28 +357,34 @@ def bench_read_ceiling(args, torch, neo):
             hip.destroy(a)
             hip.destroy(b)
         return [round(nbytes / (m * 1e-3) / 1e9, 1) for m in ms]
-    rates = {}
+    rates, b2b = {}, {}
     for nt in (True, False):
-        rates["strided_" + ("nontemporal" if nt else "plain")] = rate(
-            lambda: neo.read_probe(src, sink, nontemporal=nt))
+        key = "strided_" + ("nontemporal" if nt else "plain")
+        rates[key] = rate(lambda: neo.read_probe(src, sink, nontemporal=nt))
+        b2b[key] = back_to_back(lambda: neo.read_probe(src, sink, nontemporal=nt))
     # Waves per CU that the kernel's registers allow at each depth (51, 107,
     # 144 and 175 VGPRs: 8, 4, 3 and 2 waves per SIMD).
     fits = {1: (4, 8, 12, 16), 2: (4, 8, 12, 16), 3: (4, 8, 12), 4: (4, 8)}
     for depth, wpcs in fits.items():
         for wpc in wpcs:
-            rates[f"tiles_w{wpc}_d{depth}"] = rate(
-                lambda: neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth))
-            log(f"[bench] tile probe {wpc} waves/CU depth {depth}: "
-                f"{pct(rates[f'tiles_w{wpc}_d{depth}'], (50,))[0]} GB/s")
+            key = f"tiles_w{wpc}_d{depth}"
+
+            def fn(wpc=wpc, depth=depth):
+                neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth)
+            b2b[key] = back_to_back(fn)
+            rates[key] = rate(fn)
+            log(f"[bench] tile probe {wpc} waves/CU depth {depth}: back to back {b2b[key]} GB/s, "
+                f"one call at a time {pct(rates[key], (50,))[0]} GB/s (median)")
     med = {k: pct(v, (50,))[0] for k, v in rates.items()}
-    best_key = max(med, key=med.get)
+    best_key = max(b2b, key=b2b.get)
     print(json.dumps({
         "metric": "device read rate (measured read ceiling for HBM-bound kernels)",
-        "value": med[best_key], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+        "value": b2b[best_key], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
         "bytes": nbytes, "best_pattern": best_key,
-        "decode_pattern_gbs": med["tiles_w4_d1"], "median_gbs": med, "runs_gbs": rates,
-        "roofline": {"bound": "hbm", "achieved": med[best_key], "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(med[best_key] / PEAK_HBM_GBS, 4)},
+        "decode_pattern_gbs": b2b["tiles_w4_d1"], "back_to_back_gbs": b2b,
+        "single_call_median_gbs": med, "single_call_runs_gbs": rates,
+        "roofline": {"bound": "hbm", "achieved": b2b[best_key], "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(b2b[best_key] / PEAK_HBM_GBS, 4)},
     }), flush=True)
     return 0
 
