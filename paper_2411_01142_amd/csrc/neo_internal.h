@@ -51,10 +51,13 @@ __host__ __device__ inline int32_t pair_cost(int32_t nb) {
 // Workgroups are dispatched round-robin over the XCDs in index order (the
 // hardware XCC id read back was workgroup index mod 8 in every run), and
 // workgroup w holds slices 4w .. 4w+3, so slice s runs on XCD (s / 4) mod 8.
-// Measured on MI355X: waves on the odd-numbered XCDs stream 5-8 % slower, so
-// with equal slices they end last; 34 : 30 units gain 0.9 points on a
-// 256-request lognormal mix and 1.2 on a 70B layer, while on short slices
-// (43 tiles, batch 64) any weighting measured 0.7-1.0 points slower.
+// Measured on MI355X: waves on the odd-numbered XCDs stream 8-15 % slower per
+// tile, so with equal slices they end last. With K and V of a block in one
+// run, 34 : 30 units gain 1.3 % on a 256-request lognormal mix, 1.8 % on a 70B
+// layer, 1.0 % at batch 64 (~42 positions per slice) and 2.9 % on a 70B
+// layer's tensor-parallel share (~70); 33 : 31 and 35 : 29 measured between
+// equal slices and 34 : 30 or level with it. Slices below 16 positions are
+// dominated by their fixed costs and stay equal.
 //
 // Evaluated without 64-bit division, which the GPU has no instruction for
 // (the software sequence would run at every pair transition and merge): with
@@ -63,7 +66,7 @@ __host__ __device__ inline int32_t pair_cost(int32_t nb) {
 // one exact integer step corrects it.
 constexpr int32_t kXcdEvenUnits = 34;
 constexpr int32_t kXcdOddUnits = 30;
-constexpr int32_t kXcdWeightMinTiles = 128;
+constexpr int32_t kXcdWeightMinTiles = 16;
 constexpr int32_t kXcdPeriodUnits = 4 * (kXcdEvenUnits + kXcdOddUnits);  // 8 slices
 struct SliceGeom {
   int32_t W, n;      // positions and slices, 0 < n <= min(W, NEO_MAX_SLICES) (n = 0: no slices)

@@ -364,13 +364,14 @@ def test_group_merge_mixes_contributor_counts(variant):
 @pytest.mark.parametrize("variant", ["valu", "mfma"])
 def test_xcd_weighted_slices(variant):
     # On a part with eight XCDs, slice counts that are multiples of 8 with at
-    # least 128 positions per slice weigh the slices by XCD (34 : 30 units):
-    # 8 and 16 slices here (~300 and ~150 positions), 24 slices stay equal
-    # (~100). Every schedule must match the oracle and each other bit for bit.
+    # least 16 positions per slice weigh the slices by XCD (34 : 30 units):
+    # 8, 16 and 24 slices here (~300, ~150 and ~100 positions), 256 slices
+    # stay equal (~9). Every schedule must match the oracle and each other bit
+    # for bit.
     lens = [3000, 40, 5000, 16, 2500, 7000, 1, 1257]
     case = W.build_case(lens, 8, 2, 128, 16, seed=37)
     ref = oracle.decode_attention(case)
-    for slices in (8, 16, 24):
+    for slices in (8, 16, 24, 256):
         a = run(case, variant=variant, schedule="fused", max_slices=slices)
         b = run(case, variant=variant, schedule="two_kernel", max_slices=slices)
         c = run(case, variant=variant, schedule="staged", max_slices=slices)
