@@ -316,7 +316,8 @@ def bench_read_ceiling(args, torch, neo):
     buffer), nontemporal and plain loads; and the tile probe, the decode
     kernel's own pattern without its arithmetic (contiguous 8 KiB steps per
     wave through 4 KiB buffer resources, nontemporal), over a sweep of waves per
-    compute unit and steps in flight. Each configuration is timed two ways: its
+    compute unit and steps in flight, with equal per-wave ranges and with
+    ranges weighted by XCD. Each configuration is timed two ways: its
     calls back to back between two events (as the decode benchmark's timed
     region runs), and one call at a time with the device idle in between (the
     median of those). The best back-to-back rate is the measured read ceiling:
@@ -365,23 +366,26 @@ def bench_read_ceiling(args, torch, neo):
     # Waves per CU that the kernel's registers allow at each depth (51, 107,
     # 144 and 175 VGPRs: 8, 4, 3 and 2 waves per SIMD).
     fits = {1: (4, 8, 12, 16), 2: (4, 8, 12, 16), 3: (4, 8, 12), 4: (4, 8)}
-    for depth, wpcs in fits.items():
-        for wpc in wpcs:
-            key = f"tiles_w{wpc}_d{depth}"
+    # Each with equal per-wave ranges and with ranges weighted by XCD as the
+    # decode kernel weighs its slices (suffix _xcd): waves on odd-numbered XCDs
+    # read more slowly, so equal ranges end when those do.
+    configs = [(w, d, c) for w in (False, True) for d, cs in fits.items() for c in cs]
+    for weighted, depth, wpc in configs:
+        key = f"tiles_w{wpc}_d{depth}" + ("_xcd" if weighted else "")
 
-            def fn(wpc=wpc, depth=depth):
-                neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth)
-            b2b[key] = back_to_back(fn)
-            rates[key] = rate(fn)
-            log(f"[bench] tile probe {wpc} waves/CU depth {depth}: back to back {b2b[key]} GB/s, "
-                f"one call at a time {pct(rates[key], (50,))[0]} GB/s (median)")
+        def fn(wpc=wpc, depth=depth, weighted=weighted):
+            neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth, xcd_weighted=weighted)
+        b2b[key] = back_to_back(fn)
+        rates[key] = rate(fn)
+        log(f"[bench] tile probe {key}: back to back {b2b[key]} GB/s, "
+            f"one call at a time {pct(rates[key], (50,))[0]} GB/s (median)")
     med = {k: pct(v, (50,))[0] for k, v in rates.items()}
     best_key = max(b2b, key=b2b.get)
     print(json.dumps({
         "metric": "device read rate (measured read ceiling for HBM-bound kernels)",
         "value": b2b[best_key], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
         "bytes": nbytes, "best_pattern": best_key,
-        "decode_pattern_gbs": b2b["tiles_w4_d1"], "back_to_back_gbs": b2b,
+        "decode_pattern_gbs": b2b["tiles_w4_d1_xcd"], "back_to_back_gbs": b2b,
         "single_call_median_gbs": med, "single_call_runs_gbs": rates,
         "roofline": {"bound": "hbm", "achieved": b2b[best_key], "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(b2b[best_key] / PEAK_HBM_GBS, 4)},

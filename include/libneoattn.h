@@ -298,17 +298,22 @@ neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, ui
 /*
  * Measurement aid, not part of attention: the read rate of the decode kernel's
  * own access pattern without its arithmetic. `bytes` (a positive multiple of
- * 8192) at `src` (device memory, 256-byte aligned) are cut into 8 KiB steps
- * (two 4 KiB tiles, like the K and V tiles of one block), the steps into one
- * contiguous range per wavefront; waves_per_cu (4, 8, 12 or 16) wavefronts per
- * compute unit in workgroups of four, each with `depth` (1-4) steps in flight
- * ahead of the one it consumes; 16-byte nontemporal buffer loads. Writes one
- * word per wavefront (compute units * waves_per_cu words, at most 4096 on
- * MI355X) to `sink`: the xor of every 32-bit word that wave read, so the xor
- * of all of them is the xor of the buffer. One kernel on `stream`.
+ * 8192, below 2^44) at `src` (device memory, 256-byte aligned) are cut into
+ * 8 KiB steps (two 4 KiB tiles, like the K and V tiles of one block), the
+ * steps into one contiguous range per wavefront; waves_per_cu (4, 8, 12 or 16)
+ * wavefronts per compute unit in workgroups of four, each with `depth` (1-4)
+ * steps in flight ahead of the one it consumes; 16-byte nontemporal buffer
+ * loads. xcd_weighted = 1: on a part with eight XCDs the ranges are weighted
+ * by XCD as the decode kernel weighs its slices (34 units for a wave on an
+ * even-numbered XCD, 30 on an odd one, when the geometry allows it); 0: equal
+ * ranges. Writes one word per wavefront (compute units * waves_per_cu words,
+ * at most 4096 on MI355X) to `sink`: the xor of every 32-bit word that wave
+ * read, so the xor of all of them is the xor of the buffer. One kernel on
+ * `stream`.
  */
 neo_status neo_read_probe_tiles(const void* src, size_t bytes, int32_t waves_per_cu,
-                                int32_t depth, uint32_t* sink, size_t sink_words, void* stream);
+                                int32_t depth, int32_t xcd_weighted, uint32_t* sink,
+                                size_t sink_words, void* stream);
 
 /*
  * Decode attention on the host CPU over a KV cache in host memory (the CPU

@@ -105,7 +105,7 @@ def load_library():
         lib.neo_kv_copy_blocks.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, L, L, P]
         lib.neo_read_probe.argtypes = [P, S, I, P, S, P]
         lib.neo_read_probe.restype = ctypes.c_int
-        lib.neo_read_probe_tiles.argtypes = [P, S, I, I, P, S, P]
+        lib.neo_read_probe_tiles.argtypes = [P, S, I, I, I, P, S, P]
         lib.neo_read_probe_tiles.restype = ctypes.c_int
         lib.neo_kv_copy_blocks.restype = ctypes.c_int
         lib.neo_cpu_decode_attention_ex.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, I, I]
@@ -437,12 +437,14 @@ def read_probe(src, sink, *, nontemporal: bool = True, stream=None):
                                   sink.numel() * sink.element_size() // 4, sh))
 
 
-def read_probe_tiles(src, sink, *, waves_per_cu: int = 4, depth: int = 1, stream=None):
+def read_probe_tiles(src, sink, *, waves_per_cu: int = 4, depth: int = 1,
+                     xcd_weighted: bool = False, stream=None):
     """Read the GPU tensor ``src`` (its bytes, a multiple of 8192) once in the
     decode kernel's pattern (contiguous 8 KiB steps per wave, ``waves_per_cu``
-    waves per compute unit, ``depth`` steps in flight) and write one xor word
-    per wave into ``sink`` (``READ_PROBE_SINK_WORDS`` 32-bit words suffice).
-    Runs on ``stream`` without synchronising."""
+    waves per compute unit, ``depth`` steps in flight; ``xcd_weighted``: the
+    ranges weighted by XCD like the decode kernel's slices) and write one xor
+    word per wave into ``sink`` (``READ_PROBE_SINK_WORDS`` 32-bit words
+    suffice). Runs on ``stream`` without synchronising."""
     torch = _torch()
     lib = load_library()
     if not (src.is_cuda and sink.is_cuda) or not src.is_contiguous() or not sink.is_contiguous():
@@ -450,7 +452,8 @@ def read_probe_tiles(src, sink, *, waves_per_cu: int = 4, depth: int = 1, stream
     sh = _stream_handle(stream, src.device)
     with torch.cuda.device(src.device):
         _check(lib.neo_read_probe_tiles(src.data_ptr(), src.numel() * src.element_size(),
-                                        int(waves_per_cu), int(depth), sink.data_ptr(),
+                                        int(waves_per_cu), int(depth), int(bool(xcd_weighted)),
+                                        sink.data_ptr(),
                                         sink.numel() * sink.element_size() // 4, sh))
 
 

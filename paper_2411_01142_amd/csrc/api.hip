@@ -564,11 +564,14 @@ neo_status neo_read_probe(const void* src, size_t bytes, int32_t nontemporal, ui
 }
 
 neo_status neo_read_probe_tiles(const void* src, size_t bytes, int32_t waves_per_cu,
-                                int32_t depth, uint32_t* sink, size_t sink_words, void* stream) {
+                                int32_t depth, int32_t xcd_weighted, uint32_t* sink,
+                                size_t sink_words, void* stream) {
   if (!src || !sink) return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
-  if (bytes == 0 || bytes % 8192 != 0)
-    return set_error(NEO_ERR_INVALID_ARG, "bytes (%zu) must be a positive multiple of 8192",
-                     bytes);
+  if (bytes == 0 || bytes % 8192 != 0 || bytes / 8192 >= ((size_t)1 << 31))
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "bytes (%zu) must be a positive multiple of 8192 below 2^44", bytes);
+  if (xcd_weighted != 0 && xcd_weighted != 1)
+    return set_error(NEO_ERR_INVALID_ARG, "xcd_weighted must be 0 or 1");
   if (!aligned(src, 256)) return set_error(NEO_ERR_INVALID_ARG, "src must be 256-byte aligned");
   if (waves_per_cu < 4 || waves_per_cu > 16 || waves_per_cu % 4 != 0)
     return set_error(NEO_ERR_INVALID_ARG, "waves_per_cu %d must be 4, 8, 12 or 16",
@@ -582,8 +585,10 @@ neo_status neo_read_probe_tiles(const void* src, size_t bytes, int32_t waves_per
   if (sink_words < waves)
     return set_error(NEO_ERR_INVALID_ARG, "sink holds %zu words, needs %zu", sink_words, waves);
   const hipError_t e =
-      neo::launch_read_probe_tiles(src, bytes / 8192, (int32_t)(waves / neo::kWavesPerGroup),
-                                   depth, sink, static_cast<hipStream_t>(stream));
+      neo::launch_read_probe_tiles(src, (int32_t)(bytes / 8192),
+                                   (int32_t)(waves / neo::kWavesPerGroup), depth,
+                                   xcd_weighted != 0 && xcds == 8, sink,
+                                   static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "probe launch: %s", hipGetErrorString(e));
   return ok();
 }

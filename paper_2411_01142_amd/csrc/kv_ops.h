@@ -26,9 +26,10 @@ constexpr int kReadProbeWaves = kReadProbeBlocks * 4;
 hipError_t launch_read_probe(const void* src, size_t n16, bool nontemporal, uint32_t* sink,
                              hipStream_t stream);
 // Tile-pattern probe: nsteps 8 KiB steps split into contiguous per-wave
-// ranges over `workgroups` 4-wave workgroups, `depth` (1-4) steps in flight;
-// sink gets one word per wave (workgroups * 4).
-hipError_t launch_read_probe_tiles(const void* src, size_t nsteps, int32_t workgroups,
-                                   int32_t depth, uint32_t* sink, hipStream_t stream);
+// ranges over `workgroups` 4-wave workgroups (equal, or weighted by XCD like
+// the decode kernel's slices when xcd8), `depth` (1-4) steps in flight; sink
+// gets one word per wave (workgroups * 4).
+hipError_t launch_read_probe_tiles(const void* src, int32_t nsteps, int32_t workgroups,
+                                   int32_t depth, bool xcd8, uint32_t* sink, hipStream_t stream);
 
 }  // namespace neo

@@ -159,16 +159,19 @@ __global__ __launch_bounds__(256) void read_probe_kernel(const probe_u32x4* __re
 // instruction), kDepth steps in flight ahead of the one consumed; a step past
 // the wave's range gets resources of size 0 (its loads return zeros without
 // touching memory), so every step issues the same loads. Workgroups of four
-// waves. The wave's xor goes to sink[wave].
+// waves. The wave's xor goes to sink[wave]. xcd8: the ranges are cut by the
+// decode kernel's slice geometry with its XCD weights (waves on even XCDs get
+// 34 units, those on odd XCDs 30, where the geometry allows it), else equal.
 template <int kDepth>
 __global__ __launch_bounds__(256) void read_probe_tiles_kernel(const uint16_t* __restrict__ src,
-                                                               int64_t nsteps,
+                                                               int32_t nsteps, int32_t xcd8,
                                                                uint32_t* __restrict__ sink) {
   constexpr int kStepElems = 2 * kTileElems;  // 8 KiB of bf16
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wave = (int64_t)blockIdx.x * kWavesPerGroup + uniform(threadIdx.x >> 6);
-  const int64_t nw = (int64_t)gridDim.x * kWavesPerGroup;
-  const int64_t s0 = nsteps * wave / nw, s1 = nsteps * (wave + 1) / nw;
+  const int32_t wave = (int32_t)blockIdx.x * kWavesPerGroup + uniform(threadIdx.x >> 6);
+  const int32_t nw = (int32_t)gridDim.x * kWavesPerGroup;
+  const SliceGeom geo = make_slice_geom(nsteps, nw, xcd8 != 0);
+  const int64_t s0 = uniform(slice_start(wave, geo)), s1 = uniform(slice_start(wave + 1, geo));
   u32x4_t buf[kDepth + 1][8];
   auto issue = [&](u32x4_t(&b)[8], int64_t s) {
     const bool valid = s < s1;
@@ -202,15 +205,15 @@ __global__ __launch_bounds__(256) void read_probe_tiles_kernel(const uint16_t* _
 
 }  // namespace
 
-hipError_t launch_read_probe_tiles(const void* src, size_t nsteps, int32_t workgroups,
-                                   int32_t depth, uint32_t* sink, hipStream_t stream) {
+hipError_t launch_read_probe_tiles(const void* src, int32_t nsteps, int32_t workgroups,
+                                   int32_t depth, bool xcd8, uint32_t* sink, hipStream_t stream) {
   const uint16_t* s = static_cast<const uint16_t*>(src);
-  const int64_t n = (int64_t)nsteps;
+  const int32_t w = xcd8 ? 1 : 0;
   switch (depth) {
-    case 1: read_probe_tiles_kernel<1><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
-    case 2: read_probe_tiles_kernel<2><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
-    case 3: read_probe_tiles_kernel<3><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
-    default: read_probe_tiles_kernel<4><<<workgroups, 256, 0, stream>>>(s, n, sink); break;
+    case 1: read_probe_tiles_kernel<1><<<workgroups, 256, 0, stream>>>(s, nsteps, w, sink); break;
+    case 2: read_probe_tiles_kernel<2><<<workgroups, 256, 0, stream>>>(s, nsteps, w, sink); break;
+    case 3: read_probe_tiles_kernel<3><<<workgroups, 256, 0, stream>>>(s, nsteps, w, sink); break;
+    default: read_probe_tiles_kernel<4><<<workgroups, 256, 0, stream>>>(s, nsteps, w, sink); break;
   }
   return hipGetLastError();
 }

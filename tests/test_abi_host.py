@@ -240,6 +240,16 @@ def test_read_probe_rejects(lib, src, nbytes, sink, words):
     assert lib.neo_last_error().decode()
 
 
+@pytest.mark.parametrize("src,nbytes,wpc,depth,weighted,sink", [
+    (None, 8192, 4, 1, 0, FAKE), (FAKE, 8192, 4, 1, 0, None), (FAKE, 4096, 4, 1, 0, FAKE),
+    (FAKE, 8192 << 31, 4, 1, 0, FAKE), (FAKE + 16, 8192, 4, 1, 0, FAKE),
+    (FAKE, 8192, 6, 1, 0, FAKE), (FAKE, 8192, 4, 5, 0, FAKE), (FAKE, 8192, 4, 1, 2, FAKE),
+])
+def test_read_probe_tiles_rejects(lib, src, nbytes, wpc, depth, weighted, sink):
+    assert lib.neo_read_probe_tiles(src, nbytes, wpc, depth, weighted, sink, 4096, None) == INVALID
+    assert lib.neo_last_error().decode()
+
+
 def test_read_probe_sink_size_matches_header():
     text = open(HEADER).read()
     assert int(re.search(r"#define NEO_READ_PROBE_SINK_WORDS (\d+)", text).group(1)) == \

@@ -49,16 +49,20 @@ def test_read_probe_binding_checks():
 
 # One step (most waves empty), a count that leaves waves with unequal ranges,
 # and several rounds of every depth's ring.
+# With XCD weights the ranges follow the decode kernel's weighted slice
+# geometry (too few steps per wave for it: equal ranges again).
 @pytest.mark.parametrize("nbytes", [8192, 8192 * 1237, 1 << 27])
 @pytest.mark.parametrize("wpc,depth", [(4, 1), (8, 2), (12, 3), (8, 4), (16, 1)])
-def test_tile_probe_reads_every_word_once(nbytes, wpc, depth):
-    print(f"[probe-tiles] bytes={nbytes} waves/CU={wpc} depth={depth}", flush=True)
+@pytest.mark.parametrize("weighted", [False, True])
+def test_tile_probe_reads_every_word_once(nbytes, wpc, depth, weighted):
+    print(f"[probe-tiles] bytes={nbytes} waves/CU={wpc} depth={depth} xcd_weighted={weighted}",
+          flush=True)
     sys.stdout.flush()
     rng = np.random.default_rng(nbytes + wpc + depth)
     host = rng.integers(0, 2 ** 32, nbytes // 4, dtype=np.uint32)
     src = torch.from_numpy(host.view(np.int32)).cuda()
     sink = torch.zeros(neo.READ_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
-    neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth)
+    neo.read_probe_tiles(src, sink, waves_per_cu=wpc, depth=depth, xcd_weighted=weighted)
     torch.cuda.synchronize()
     words = sink.cpu().numpy().view(np.uint32)
     assert np.bitwise_xor.reduce(words) == np.bitwise_xor.reduce(host)
