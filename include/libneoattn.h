@@ -199,7 +199,8 @@ neo_status neo_decode_attention_events(const void* q, const void* k_cache, const
 /*
  * For callers that cannot allocate device memory or a workspace (code under
  * HIP graph capture, tight serving loops, harnesses that forbid allocation):
- * neo_decode_attention without the workspace arguments. The same operation,
+ * neo_decode_attention without the workspace arguments, with the caches'
+ * block stride as for neo_decode_attention_ex (0: dense). The same operation,
  * layouts, checks and clamping rules, and the same single fused kernel
  * (MFMA family, default slice policy capped at 1024 slices); for a given
  * input the result equals neo_decode_attention's up to fp32 summation order
@@ -221,7 +222,8 @@ neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, cons
                                         int32_t num_q_heads, int32_t num_kv_heads,
                                         int32_t head_dim, int32_t block_size, float scale,
                                         float* out, int32_t batch, int32_t max_blocks_per_seq,
-                                        int32_t num_blocks, void* stream);
+                                        int32_t num_blocks, int64_t kv_block_stride,
+                                        void* stream);
 
 /*
  * Bit-exact dense copy of one paged cache through the block table (the paged

@@ -94,7 +94,7 @@ def load_library():
         lib.neo_decode_attention_events.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P,
                                                     S, I, I, I, L, P, P, P]
         lib.neo_decode_attention_events.restype = ctypes.c_int
-        lib.neo_decode_attention_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, P]
+        lib.neo_decode_attention_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, F, P, I, I, I, L, P]
         lib.neo_decode_attention_noalloc.restype = ctypes.c_int
         lib.neo_decode_workspace_init.argtypes = [P, S, P]
         lib.neo_decode_workspace_init.restype = ctypes.c_int

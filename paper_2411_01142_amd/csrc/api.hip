@@ -374,12 +374,13 @@ neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, cons
                                         int32_t num_q_heads, int32_t num_kv_heads,
                                         int32_t head_dim, int32_t block_size, float scale,
                                         float* out, int32_t batch, int32_t max_blocks_per_seq,
-                                        int32_t num_blocks, void* stream) {
+                                        int32_t num_blocks, int64_t kv_block_stride,
+                                        void* stream) {
   bool noop = false;
   neo_status st = check_decode(q, k_cache, v_cache, block_table, seq_lens, num_q_heads,
                                num_kv_heads, head_dim, block_size, scale, out, batch,
                                max_blocks_per_seq, num_blocks, NEO_VARIANT_AUTO,
-                               NEO_SCHEDULE_AUTO, 0, 0, &noop);
+                               NEO_SCHEDULE_AUTO, 0, kv_block_stride, &noop);
   if (st != NEO_OK || noop) return st;
   const int32_t group = num_q_heads / num_kv_heads;
   if (group > kScratchMaxGroup)
@@ -418,7 +419,7 @@ neo_status neo_decode_attention_noalloc(const void* q, const void* k_cache, cons
   p.slice_quantum = quantum;
   p.xcd8 = xcds == 8;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.blk_stride = (int64_t)num_kv_heads * neo::kTileElems;
+  p.blk_stride = kv_block_stride != 0 ? kv_block_stride : (int64_t)num_kv_heads * neo::kTileElems;
   const int32_t grid = (slices + neo::kWavesPerGroup - 1) / neo::kWavesPerGroup;
   const hipError_t e = neo::launch_decode_mfma(p, group, neo::kFused, grid, s);
   if (e != hipSuccess) return set_error(NEO_ERR_HIP, "decode launch: %s", hipGetErrorString(e));

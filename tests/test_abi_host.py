@@ -278,13 +278,16 @@ def test_noalloc_entry_point_checks_arguments_before_any_hip_call(lib):
         a.update(kw)
         return lib.neo_decode_attention_noalloc(a["q"], a["k"], a["v"], a["table"], a["lens"],
                                                 a["hq"], a["hkv"], a["d"], a["bs"], a["scale"],
-                                                a["out"], a["batch"], a["mbps"], a["nb"], None)
+                                                a["out"], a["batch"], a["mbps"], a["nb"],
+                                                a.get("stride", 0), None)
     assert na(hkv=7) == INVALID
     assert na(d=64) == UNSUPPORTED
     assert na(bs=8) == UNSUPPORTED
     assert na(scale=float("nan")) == INVALID
     assert na(out=None) == INVALID
     assert na(q=FAKE + 4) == INVALID
+    assert na(stride=8 * 2048 - 8) == INVALID
+    assert na(stride=2 * 8 * 2048 + 4) == INVALID
     assert na(batch=0, q=None, k=None, v=None, table=None, lens=None, out=None) == OK
 
 
