@@ -41,8 +41,9 @@
  * live in one allocation [num_blocks][K, V][num_kv_heads][tile], each block's
  * K and V in one run of 2 * num_kv_heads * 4 KiB (interleaved caches). On
  * MI355X decode attention streams such caches 1-6 % faster than two separate
- * allocations: the HBM read rate drops as a block's K and V tiles lie further
- * apart.
+ * allocations: the HBM read rate depends on where a block's K and V tiles lie
+ * relative to each other, and of the placements measured this one (without
+ * padding) was the fastest.
  *
  * Supported: head_dim 128, block_size 16, num_q_heads / num_kv_heads in {1,2,4,8,16}.
  * q, k_cache, v_cache and out must be 16-byte aligned; the workspace 256-byte aligned.
@@ -165,7 +166,8 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
  * (1 = no request is ever split). kv_block_stride: elements from one block to
  * the next in k_cache and in v_cache (see "Block stride" above); 0 means
  * num_kv_heads * head_dim * block_size (dense caches); otherwise a multiple
- * of 8 of at least that (NEO_ERR_INVALID_ARG). The caller's caches must hold
+ * of 8 of at least that and at most 2^40 (NEO_ERR_INVALID_ARG). The caller's
+ * caches must hold
  * num_blocks blocks at that stride. The result is the same operation for
  * every choice, up to fp32 summation order, and bit for bit the same for
  * every block stride.
