@@ -167,10 +167,9 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
  * the next in k_cache and in v_cache (see "Block stride" above); 0 means
  * num_kv_heads * head_dim * block_size (dense caches); otherwise a multiple
  * of 8 of at least that and at most 2^40 (NEO_ERR_INVALID_ARG). The caller's
- * caches must hold
- * num_blocks blocks at that stride. The result is the same operation for
- * every choice, up to fp32 summation order, and bit for bit the same for
- * every block stride.
+ * caches must hold num_blocks blocks at that stride. The result is the same
+ * operation for every choice, up to fp32 summation order, and bit for bit the
+ * same for every block stride.
  */
 neo_status neo_decode_attention_ex(const void* q, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* seq_lens,
