@@ -166,7 +166,8 @@ neo_status neo_decode_attention(const void* q, const void* k_cache, const void* 
  * (1 = no request is ever split). kv_block_stride: elements from one block to
  * the next in k_cache and in v_cache (see "Block stride" above); 0 means
  * num_kv_heads * head_dim * block_size (dense caches); otherwise a multiple
- * of 8 of at least that and at most 2^40 (NEO_ERR_INVALID_ARG). The caller's
+ * of 8 of at least that and at most 2^40, with num_blocks blocks at that
+ * stride spanning less than 2^62 bytes (NEO_ERR_INVALID_ARG). The caller's
  * caches must hold num_blocks blocks at that stride. The result is the same
  * operation for every choice, up to fp32 summation order, and bit for bit the
  * same for every block stride.

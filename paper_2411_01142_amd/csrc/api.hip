@@ -122,6 +122,16 @@ neo_status check_block_stride(int64_t stride, int64_t dense, const char* name,
   return NEO_OK;
 }
 
+// The caches' byte span (num_blocks blocks at `stride` elements) must stay far
+// inside 64 bits, so that no block offset the kernels form can wrap.
+neo_status check_span(int64_t stride, int32_t num_blocks, const char* name) {
+  if (num_blocks > 0 && stride > (((int64_t)1 << 61) / num_blocks))
+    return set_error(NEO_ERR_INVALID_ARG,
+                     "%s: %d blocks at a stride of %lld elements span 2^62 bytes or more",
+                     name, num_blocks, (long long)stride);
+  return NEO_OK;
+}
+
 // Host-side checks of a decode call, shared by every decode entry point (no
 // HIP call). *noop is set for an empty batch, which needs no pointer.
 neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
@@ -161,6 +171,10 @@ neo_status check_decode(const void* q, const void* k_cache, const void* v_cache,
     return set_error(NEO_ERR_INVALID_ARG,
                      "max_blocks_per_seq (%d) and num_blocks (%d) must be positive",
                      max_blocks_per_seq, num_blocks);
+  {
+    const neo_status span = check_span(resolved, num_blocks, "kv_block_stride");
+    if (span != NEO_OK) return span;
+  }
   if ((int64_t)batch * (max_blocks_per_seq + neo::kPairCostLong) * num_kv_heads >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG,
                      "batch * (max_blocks_per_seq + %d) * num_kv_heads must stay below 2^31",
@@ -456,6 +470,10 @@ neo_status neo_paged_gather(const void* cache, int32_t is_v, const int32_t* bloc
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  {
+    const neo_status span = check_span(stride, num_blocks, "block_stride");
+    if (span != NEO_OK) return span;
+  }
   if (batch > 65535) return set_error(NEO_ERR_INVALID_ARG, "batch above 65535");
   if ((int64_t)max_blocks_per_seq * block_size >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
@@ -486,6 +504,10 @@ neo_status neo_kv_append(void* k_cache, void* v_cache, const void* k_new, const 
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (max_blocks_per_seq <= 0 || num_blocks <= 0)
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be positive");
+  {
+    const neo_status span = check_span(stride, num_blocks, "kv_block_stride");
+    if (span != NEO_OK) return span;
+  }
   if ((int64_t)max_blocks_per_seq * neo::kBlock >= ((int64_t)1 << 31))
     return set_error(NEO_ERR_INVALID_ARG, "max_blocks_per_seq too large");
   if ((int64_t)batch * num_kv_heads >= ((int64_t)1 << 31))
@@ -522,6 +544,10 @@ neo_status neo_kv_copy_blocks(const void* src_k, const void* src_v, void* dst_k,
     return set_error(NEO_ERR_INVALID_ARG, "a required pointer is NULL");
   if (src_num_blocks <= 0 || dst_num_blocks <= 0)
     return set_error(NEO_ERR_INVALID_ARG, "block counts must be positive");
+  sst = check_span(src_stride, src_num_blocks, "src_block_stride");
+  if (sst != NEO_OK) return sst;
+  sst = check_span(dst_stride, dst_num_blocks, "dst_block_stride");
+  if (sst != NEO_OK) return sst;
   if (!aligned(src_k, 16) || !aligned(src_v, 16) || !aligned(dst_k, 16) || !aligned(dst_v, 16))
     return set_error(NEO_ERR_INVALID_ARG, "caches must be 16-byte aligned");
   // Every pointer the kernel dereferences must be device memory or pinned host

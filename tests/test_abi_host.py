@@ -144,6 +144,7 @@ def call(lib, **kw):
     (dict(kv_stride=2 * 8 * 2048 + 4), INVALID, "kv_block_stride"),
     (dict(kv_stride=-2048), INVALID, "kv_block_stride"),
     (dict(kv_stride=1 << 41), INVALID, "kv_block_stride"),
+    (dict(kv_stride=1 << 40, nb=1 << 22), INVALID, "kv_block_stride"),  # span of 2^62+ bytes
 ])
 def test_decode_rejects_bad_arguments_before_any_hip_call(lib, kw, code, needle):
     assert call(lib, **kw) == code
@@ -197,7 +198,7 @@ def append_call(lib, **kw):
     (dict(k=FAKE + 2), INVALID), (dict(kn=FAKE + 8), INVALID), (dict(v=FAKE + 1), INVALID),
     (dict(mbps=1 << 28), INVALID), (dict(batch=1 << 28, hkv=16), INVALID),
     (dict(stride=8 * 2048 - 8), INVALID), (dict(stride=8 * 2048 + 2), INVALID),
-    (dict(stride=-1), INVALID),
+    (dict(stride=-1), INVALID), (dict(stride=1 << 40, nb=1 << 22), INVALID),
 ])
 def test_kv_append_rejects(lib, kw, code):
     assert append_call(lib, **kw) == code
@@ -224,7 +225,8 @@ def copy_call(lib, **kw):
     (dict(di=None), INVALID), (dict(snb=0), INVALID), (dict(dnb=-5), INVALID),
     (dict(sv=FAKE + 8), INVALID), (dict(dk=FAKE + 4), INVALID),
     (dict(sst=8 * 2048 - 8), INVALID), (dict(dst=2 * 8 * 2048 + 6), INVALID),
-    (dict(dst=(1 << 40) + 8), INVALID),
+    (dict(dst=(1 << 40) + 8), INVALID), (dict(sst=1 << 40, snb=1 << 22), INVALID),
+    (dict(dst=1 << 39, dnb=1 << 23), INVALID),
 ])
 def test_kv_copy_blocks_rejects(lib, kw, code):
     assert copy_call(lib, **kw) == code
