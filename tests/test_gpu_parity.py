@@ -440,7 +440,8 @@ def test_random_shapes(i):
 def mixed_random_case(i):
     """Shapes beyond the power-of-two kv head counts (3, 5, 16 kv heads), lengths
     around block multiples, runs of 0-1 token requests, equal lengths, a few long
-    requests among short ones; random kernel family, launch schedule and slice cap."""
+    requests among short ones; random kernel family, launch schedule, slice cap
+    and cache layout (two caches, or both in one buffer with or without padding)."""
     rng = np.random.default_rng(90000 + i)
     hkv = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
     group = int(rng.choice([1, 2, 4, 8, 16]))
@@ -468,16 +469,19 @@ def mixed_random_case(i):
     variant = str(rng.choice(["mfma", "mfma", "valu"]))
     schedule = str(rng.choice(["fused", "fused", "staged", "two_kernel"]))
     slices = int(rng.choice([0, 0, 0, 1, 2, 5, 63, 200, 777, 1024, 2048, 4096]))
-    return case, variant, schedule, slices
+    layout = str(rng.choice(["separate", "interleaved"]))
+    pad = int(rng.choice([0, 0, 8, 1024])) if layout == "interleaved" else 0
+    return case, variant, schedule, slices, layout, pad
 
 
 @pytest.mark.parametrize("i", range(60))
 def test_mixed_random_shapes_and_launches(i):
-    case, variant, schedule, slices = mixed_random_case(i)
+    case, variant, schedule, slices, layout, pad = mixed_random_case(i)
     say(f"[mixed] case {i}: B={case.batch} Hq={case.num_q_heads} Hkv={case.num_kv_heads} "
-        f"sumL={case.total_tokens()} {variant} {schedule} slices={slices}")
+        f"sumL={case.total_tokens()} {variant} {schedule} slices={slices} {layout} pad={pad}")
     ref = oracle.decode_attention(case)
-    assert_parity(run(case, variant=variant, schedule=schedule, max_slices=slices), ref,
+    assert_parity(run(case, variant=variant, schedule=schedule, max_slices=slices,
+                      kv_layout=layout, kv_pad=pad), ref,
                   f"mixed random {i}")
 
 
