@@ -40,3 +40,17 @@ def test_counted_traffic_is_close_to_the_algorithmic_bytes(path):
     reads = rec["fetch_kib_per_launch"] * 1024 * rec["copy_factor_fetch"]
     assert 0.99 <= ratio <= 1.05, ratio
     assert reads <= 1.02 * rec["algorithmic_bytes_per_launch"]
+
+
+TRACES = sorted(glob.glob(os.path.join(ROOT, "profiles", "decode_mfma_fused__*__kernel_trace.md")))
+
+
+@pytest.mark.parametrize("path", TRACES, ids=[os.path.basename(p) for p in TRACES])
+def test_trace_mean_agrees_with_the_bench_figure_of_the_same_run(path):
+    # The decode kernel's mean duration over the timed region in rocprofv3's
+    # kernel trace against bench.py's own event-timed kernel_ms of that run.
+    text = open(path).read()
+    bench_us = float(re.search(r"`roofline\.kernel_ms` =\s*([0-9.]+) us", text).group(1))
+    trace_us = float(re.search(r"From the trace: [0-9.]+ MB / ([0-9.]+) us", text).group(1))
+    assert abs(trace_us - bench_us) <= 0.015 * bench_us, (trace_us, bench_us)
+    assert "rocprofv3 --kernel-trace --stats" in text
